@@ -1,0 +1,318 @@
+"""ctypes binding of libdas.so (include/das.h).
+
+Argument marshalling only: tensors are checked for device, dtype, shape and
+contiguity, their device pointers and the current HIP stream are passed to
+the C ABI, and a non-zero status raises DasError. Every computation runs in
+the library's HIP kernels; there is no fallback. Importing this module
+without a built library raises, so a missing extension fails loudly.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from ctypes import POINTER, c_char_p, c_int32, c_size_t, c_uint32, c_void_p
+from dataclasses import dataclass, field
+from typing import Dict, Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libdas.so")
+
+MAX_DEPTH = 64
+PAGE_TOKENS = 64
+MAX_BLOCK = 64
+
+DAS_OK = 0
+STATUS_NAMES = {0: "DAS_OK", -1: "DAS_ERR_NULL", -2: "DAS_ERR_SHAPE", -3: "DAS_ERR_DEPTH",
+                -4: "DAS_ERR_DTYPE", -5: "DAS_ERR_WORKSPACE", -6: "DAS_ERR_HIP",
+                -7: "DAS_ERR_UNSUPPORTED"}
+DTYPE_CODES = {torch.float32: 0, torch.bfloat16: 1}
+PATHS = {"auto": 0, "valu": 1, "mfma": 2}
+DEVERR_PAGE, DEVERR_PREFIX, DEVERR_COMMIT = 1, 2, 4
+
+EXPORTED = ["das_attn_workspace_bytes", "das_attn_workspace_bytes_ex", "das_attn_draft_maturev",
+            "das_attn_verify", "das_attn_policy", "das_kv_append", "das_status_string",
+            "das_version"]
+
+
+class DasError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__(f"{what}: {STATUS_NAMES.get(status, status)} ({status_string(status)})")
+
+
+class DasCacheC(ctypes.Structure):
+    _fields_ = [("dtype", c_int32), ("num_depths", c_int32), ("num_layers", c_int32),
+                ("num_kv_heads", c_int32), ("head_dim", c_int32), ("num_pages", c_int32),
+                ("num_k_planes", c_int32), ("num_v_planes", c_int32),
+                ("k_plane", c_int32 * (MAX_DEPTH + 1)), ("v_plane", c_int32 * (MAX_DEPTH + 1)),
+                ("k_pool", c_void_p), ("v_pool", c_void_p)]
+
+
+class DasBatchC(ctypes.Structure):
+    _fields_ = [("batch", c_int32), ("max_pages_per_seq", c_int32), ("prefix_len", c_void_p),
+                ("block_table", c_void_p), ("dev_error", c_void_p)]
+
+
+class DasOptionsC(ctypes.Structure):
+    _fields_ = [("path", c_int32), ("pages_per_split", c_int32)]
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"libdas.so not built at {LIB_PATH}; run python -m paper_2609_34538_amd.build")
+    lib = ctypes.CDLL(LIB_PATH)
+    pc, pb, po = POINTER(DasCacheC), POINTER(DasBatchC), POINTER(DasOptionsC)
+    attn_args = [pc, pb, c_int32, c_int32, c_int32, c_int32, c_void_p, c_void_p, c_void_p,
+                 c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]
+    lib.das_attn_workspace_bytes.argtypes = [pc, pb, c_int32, c_int32]
+    lib.das_attn_workspace_bytes.restype = c_size_t
+    lib.das_attn_workspace_bytes_ex.argtypes = [pc, pb, c_int32, c_int32, po]
+    lib.das_attn_workspace_bytes_ex.restype = c_size_t
+    lib.das_attn_draft_maturev.argtypes = attn_args
+    lib.das_attn_draft_maturev.restype = c_int32
+    lib.das_attn_verify.argtypes = attn_args
+    lib.das_attn_verify.restype = c_int32
+    lib.das_attn_policy.argtypes = [pc, pb, c_int32, c_int32, c_int32, c_int32, c_int32,
+                                    c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
+                                    c_size_t, po, c_void_p]
+    lib.das_attn_policy.restype = c_int32
+    lib.das_kv_append.argtypes = [pc, pb, c_void_p, c_void_p, c_int32, c_void_p, c_void_p,
+                                  c_void_p]
+    lib.das_kv_append.restype = c_int32
+    lib.das_status_string.argtypes = [c_int32]
+    lib.das_status_string.restype = c_char_p
+    lib.das_version.argtypes = []
+    lib.das_version.restype = c_int32
+    return lib
+
+
+LIB = _load()
+
+
+def status_string(status: int) -> str:
+    return LIB.das_status_string(status).decode()
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream_handle(stream) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream
+
+
+@dataclass
+class PagedCache:
+    """Caller-owned depth-indexed paged cache (layouts as in das.h).
+
+    k_pool: [nK, L, Hkv, P, 64, dh]; v_pool: [nV, L, Hkv, P, dh, 64].
+    k_plane / v_plane map a depth r (1..R) to its plane index."""
+    k_pool: torch.Tensor
+    v_pool: torch.Tensor
+    num_depths: int
+    k_plane: Dict[int, int]
+    v_plane: Dict[int, int]
+    _c: DasCacheC = field(default=None, repr=False)
+
+    def __post_init__(self):
+        self.refresh()
+
+    @property
+    def num_layers(self):
+        return self.k_pool.shape[1]
+
+    @property
+    def num_kv_heads(self):
+        return self.k_pool.shape[2]
+
+    @property
+    def num_pages(self):
+        return self.k_pool.shape[3]
+
+    @property
+    def head_dim(self):
+        return self.k_pool.shape[5]
+
+    @property
+    def dtype(self):
+        return self.k_pool.dtype
+
+    def refresh(self):
+        k, v = self.k_pool, self.v_pool
+        if k.dim() != 6 or v.dim() != 6:
+            raise ValueError("pools must be 6-d")
+        if k.shape[4] != PAGE_TOKENS or v.shape[5] != PAGE_TOKENS:
+            raise ValueError("pages hold 64 tokens")
+        if k.shape[1:4] != v.shape[1:4] or k.shape[5] != v.shape[4] or k.dtype != v.dtype:
+            raise ValueError("k_pool / v_pool disagree")
+        if not (k.is_contiguous() and v.is_contiguous()):
+            raise ValueError("pools must be contiguous")
+        c = DasCacheC()
+        c.dtype = DTYPE_CODES[k.dtype]
+        c.num_depths = self.num_depths
+        c.num_layers, c.num_kv_heads, c.num_pages = k.shape[1], k.shape[2], k.shape[3]
+        c.head_dim = k.shape[5]
+        c.num_k_planes, c.num_v_planes = k.shape[0], v.shape[0]
+        for r in range(MAX_DEPTH + 1):
+            c.k_plane[r] = self.k_plane.get(r, -1)
+            c.v_plane[r] = self.v_plane.get(r, -1)
+        c.k_pool, c.v_pool = k.data_ptr(), v.data_ptr()
+        self._c = c
+        return self
+
+    @property
+    def c(self) -> DasCacheC:
+        return self._c
+
+
+@dataclass
+class Batch:
+    """prefix_len [B] int32, block_table [B, max_pages] int32 (device), and an
+    optional device error word."""
+    prefix_len: torch.Tensor
+    block_table: torch.Tensor
+    dev_error: Optional[torch.Tensor] = None
+    _c: DasBatchC = field(default=None, repr=False)
+
+    def __post_init__(self):
+        self.refresh()
+
+    def refresh(self):
+        pl, bt = self.prefix_len, self.block_table
+        if pl.dtype != torch.int32 or bt.dtype != torch.int32:
+            raise ValueError("prefix_len and block_table are int32")
+        if bt.dim() != 2 or pl.shape != (bt.shape[0],):
+            raise ValueError("block_table must be [B, max_pages] and prefix_len [B]")
+        if not (pl.is_contiguous() and bt.is_contiguous()):
+            raise ValueError("batch arrays must be contiguous")
+        c = DasBatchC()
+        c.batch, c.max_pages_per_seq = bt.shape
+        c.prefix_len, c.block_table = pl.data_ptr(), bt.data_ptr()
+        c.dev_error = _ptr(self.dev_error)
+        self._c = c
+        return self
+
+    @property
+    def batch(self):
+        return self.block_table.shape[0]
+
+    @property
+    def c(self) -> DasBatchC:
+        return self._c
+
+
+def _options(path: str, pages_per_split: int):
+    o = DasOptionsC()
+    o.path = PATHS[path]
+    o.pages_per_split = pages_per_split
+    return o
+
+
+def workspace_bytes(cache: PagedCache, batch: Batch, num_q_heads: int, block_len: int,
+                    path: str = "auto", pages_per_split: int = 0) -> int:
+    o = _options(path, pages_per_split)
+    return LIB.das_attn_workspace_bytes_ex(ctypes.byref(cache.c), ctypes.byref(batch.c),
+                                           num_q_heads, block_len, ctypes.byref(o))
+
+
+def alloc_workspace(cache: PagedCache, batch: Batch, num_q_heads: int, block_len: int,
+                    path: str = "auto", pages_per_split: int = 0) -> torch.Tensor:
+    n = workspace_bytes(cache, batch, num_q_heads, block_len, path, pages_per_split)
+    if n == 0:
+        raise DasError(-2, "workspace query rejected the shapes")
+    return torch.empty(n, dtype=torch.uint8, device=cache.k_pool.device)
+
+
+def _check_block(cache: PagedCache, batch: Batch, q, k_blk, v_blk):
+    B, w, hq, dh = q.shape
+    if B != batch.batch or dh != cache.head_dim:
+        raise ValueError("q must be [B, w, Hq, dh]")
+    want = (B, w, cache.num_kv_heads, dh)
+    for t in (q, k_blk, v_blk):
+        if t.dtype != cache.dtype or not t.is_contiguous() or t.device != cache.k_pool.device:
+            raise ValueError("block tensors must be contiguous, on the cache's device and dtype")
+    if tuple(k_blk.shape) != want or tuple(v_blk.shape) != want:
+        raise ValueError("k_blk / v_blk must be [B, w, Hkv, dh]")
+    return w, hq
+
+
+def attn_policy(cache: PagedCache, batch: Batch, layer: int, kappa: int, nu: int,
+                q: torch.Tensor, k_blk: torch.Tensor, v_blk: torch.Tensor,
+                out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
+                workspace: Optional[torch.Tensor] = None, path: str = "auto",
+                pages_per_split: int = 0, stream=None) -> torch.Tensor:
+    """Eq. (2)-(3) with prefix keys at depth kappa and values at depth nu."""
+    w, hq = _check_block(cache, batch, q, k_blk, v_blk)
+    if out is None:
+        out = torch.empty_like(q)
+    if workspace is None:
+        workspace = alloc_workspace(cache, batch, hq, w, path, pages_per_split)
+    o = _options(path, pages_per_split)
+    st = LIB.das_attn_policy(ctypes.byref(cache.c), ctypes.byref(batch.c), layer, kappa, nu,
+                             hq, w, q.data_ptr(), k_blk.data_ptr(), v_blk.data_ptr(),
+                             out.data_ptr(), _ptr(lse), workspace.data_ptr(),
+                             workspace.numel(), ctypes.byref(o), _stream_handle(stream))
+    if st != DAS_OK:
+        raise DasError(st, "das_attn_policy")
+    return out
+
+
+def attn_draft_maturev(cache: PagedCache, batch: Batch, layer: int, draft_depth: int,
+                       q, k_blk, v_blk, out=None, lse=None, workspace=None, stream=None):
+    """Mature-V draft read: keys at draft_depth, values at the full depth R."""
+    w, hq = _check_block(cache, batch, q, k_blk, v_blk)
+    if out is None:
+        out = torch.empty_like(q)
+    if workspace is None:
+        workspace = alloc_workspace(cache, batch, hq, w)
+    st = LIB.das_attn_draft_maturev(ctypes.byref(cache.c), ctypes.byref(batch.c), layer,
+                                    draft_depth, hq, w, q.data_ptr(), k_blk.data_ptr(),
+                                    v_blk.data_ptr(), out.data_ptr(), _ptr(lse),
+                                    workspace.data_ptr(), workspace.numel(),
+                                    _stream_handle(stream))
+    if st != DAS_OK:
+        raise DasError(st, "das_attn_draft_maturev")
+    return out
+
+
+def attn_verify(cache: PagedCache, batch: Batch, layer: int, depth: int, q, k_blk, v_blk,
+                out=None, lse=None, workspace=None, stream=None):
+    """The target's aligned read at `depth` (the full-depth verifier at R)."""
+    w, hq = _check_block(cache, batch, q, k_blk, v_blk)
+    if out is None:
+        out = torch.empty_like(q)
+    if workspace is None:
+        workspace = alloc_workspace(cache, batch, hq, w)
+    st = LIB.das_attn_verify(ctypes.byref(cache.c), ctypes.byref(batch.c), layer, depth, hq,
+                             w, q.data_ptr(), k_blk.data_ptr(), v_blk.data_ptr(),
+                             out.data_ptr(), _ptr(lse), workspace.data_ptr(),
+                             workspace.numel(), _stream_handle(stream))
+    if st != DAS_OK:
+        raise DasError(st, "das_attn_verify")
+    return out
+
+
+def kv_append(cache: PagedCache, batch: Batch, k_new: torch.Tensor, v_new: torch.Tensor,
+              num_new: torch.Tensor, len_out: Optional[torch.Tensor] = None, stream=None):
+    """Commit the first num_new[b] block entries of every plane and layer."""
+    nk, L, B, w_max, hkv, dh = k_new.shape
+    if (nk, L, B, hkv, dh) != (cache.k_pool.shape[0], cache.num_layers, batch.batch,
+                               cache.num_kv_heads, cache.head_dim):
+        raise ValueError("k_new must be [nK, L, B, w_max, Hkv, dh]")
+    if tuple(v_new.shape) != (cache.v_pool.shape[0], L, B, w_max, hkv, dh):
+        raise ValueError("v_new must be [nV, L, B, w_max, Hkv, dh]")
+    for t in (k_new, v_new):
+        if t.dtype != cache.dtype or not t.is_contiguous():
+            raise ValueError("k_new / v_new must be contiguous in the cache dtype")
+    if num_new.dtype != torch.int32 or num_new.shape != (B,):
+        raise ValueError("num_new must be int32 [B]")
+    st = LIB.das_kv_append(ctypes.byref(cache.c), ctypes.byref(batch.c), k_new.data_ptr(),
+                           v_new.data_ptr(), w_max, num_new.data_ptr(), _ptr(len_out),
+                           _stream_handle(stream))
+    if st != DAS_OK:
+        raise DasError(st, "das_kv_append")

@@ -1,0 +1,262 @@
+// Host side of the DAS attention library: argument validation, split
+// planning, workspace sizing and kernel dispatch behind the C ABI of das.h.
+//
+// Every check runs before the first HIP call, so a rejected request has
+// enqueued nothing and the checks can be exercised without a GPU.
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include "das_internal.h"
+
+namespace das {
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+int elem_bytes(int dtype) { return dtype == DAS_F32 ? 4 : 2; }
+
+das_status check_cache(const das_cache *c) {
+  if (!c) return DAS_ERR_NULL;
+  if (!c->k_pool || !c->v_pool) return DAS_ERR_NULL;
+  if (c->dtype != DAS_F32 && c->dtype != DAS_BF16) return DAS_ERR_DTYPE;
+  if (c->num_depths < 1 || c->num_depths > DAS_MAX_DEPTH) return DAS_ERR_SHAPE;
+  if (c->num_layers < 1 || c->num_kv_heads < 1 || c->num_pages < 1) return DAS_ERR_SHAPE;
+  if (c->num_k_planes < 1 || c->num_v_planes < 1) return DAS_ERR_SHAPE;
+  if (c->head_dim != 64 && c->head_dim != 96 && c->head_dim != 128) return DAS_ERR_SHAPE;
+  for (int r = 1; r <= c->num_depths; ++r) {
+    if (c->k_plane[r] < -1 || c->k_plane[r] >= c->num_k_planes) return DAS_ERR_SHAPE;
+    if (c->v_plane[r] < -1 || c->v_plane[r] >= c->num_v_planes) return DAS_ERR_SHAPE;
+  }
+  return DAS_OK;
+}
+
+das_status check_batch(const das_batch *b) {
+  if (!b) return DAS_ERR_NULL;
+  if (!b->prefix_len || !b->block_table) return DAS_ERR_NULL;
+  if (b->batch < 1 || b->max_pages_per_seq < 1) return DAS_ERR_SHAPE;
+  return DAS_OK;
+}
+
+// Which kernel family runs a request.
+int choose_path(const das_cache *c, const das_attn_options *o) {
+  const int want = o ? o->path : DAS_PATH_AUTO;
+  if (c->dtype == DAS_F32) return DAS_PATH_VALU;
+  if (want == DAS_PATH_VALU || want == DAS_PATH_MFMA) return want;
+  return DAS_PATH_VALU;
+}
+
+struct Plan {
+  int path;
+  int rows;             // w * G query rows per (sequence, kv head)
+  int pages_per_split;
+  int nsplit;
+  size_t ws_o_bytes, ws_ml_bytes, total;
+};
+
+// Prefix pages of one sequence are cut into splits of pages_per_split pages;
+// each split is one workgroup (per kv head and row tile). The default aims
+// for enough workgroups to fill 256 compute units several times while
+// keeping each split long enough to amortise its partial-result traffic.
+das_status make_plan(const das_cache *c, const das_batch *b, int hq, int w,
+                     const das_attn_options *o, Plan *plan) {
+  if (hq < 1 || hq % c->num_kv_heads != 0) return DAS_ERR_SHAPE;
+  const int group = hq / c->num_kv_heads;
+  if (group > 8) return DAS_ERR_UNSUPPORTED;
+  if (w < 1 || w > DAS_MAX_BLOCK) return DAS_ERR_SHAPE;
+  if (o && (o->pages_per_split < 0 || o->path < DAS_PATH_AUTO || o->path > DAS_PATH_MFMA))
+    return DAS_ERR_SHAPE;
+  if (o && o->path == DAS_PATH_MFMA && c->dtype != DAS_BF16) return DAS_ERR_UNSUPPORTED;
+  plan->path = choose_path(c, o);
+  plan->rows = w * group;
+  const int row_tiles_unit = plan->path == DAS_PATH_MFMA ? mfma_rows_per_wg(plan->rows)
+                                                          : kValuRows;
+  const long row_tiles = (plan->rows + row_tiles_unit - 1) / row_tiles_unit;
+  const long units = static_cast<long>(b->batch) * c->num_kv_heads * row_tiles;
+  const int maxp = b->max_pages_per_seq;
+  int pps = o ? o->pages_per_split : 0;
+  if (pps == 0) {
+    const long target_wgs = 2048;
+    long want = (static_cast<long>(maxp) * units + target_wgs - 1) / target_wgs;
+    if (want < 2) want = 2;
+    pps = static_cast<int>(want);
+  }
+  if (pps > maxp) pps = maxp;
+  plan->pages_per_split = pps;
+  plan->nsplit = (maxp + pps - 1) / pps;
+  const size_t per_split_rows =
+      static_cast<size_t>(b->batch) * c->num_kv_heads * plan->nsplit * plan->rows;
+  plan->ws_o_bytes = align_up(per_split_rows * c->head_dim * sizeof(float));
+  plan->ws_ml_bytes = align_up(per_split_rows * sizeof(float));
+  plan->total = plan->ws_o_bytes + 2 * plan->ws_ml_bytes;
+  return DAS_OK;
+}
+
+das_status attn_common(const das_cache *c, const das_batch *b, int layer, int kappa, int nu,
+                       int hq, int w, const void *q, const void *kb, const void *vb, void *out,
+                       float *lse, void *ws, size_t ws_bytes, const das_attn_options *o,
+                       hipStream_t stream) {
+  das_status st = check_cache(c);
+  if (st != DAS_OK) return st;
+  st = check_batch(b);
+  if (st != DAS_OK) return st;
+  if (!q || !kb || !vb || !out) return DAS_ERR_NULL;
+  if (layer < 0 || layer >= c->num_layers) return DAS_ERR_SHAPE;
+  if (kappa < 1 || kappa > c->num_depths || nu < 1 || nu > c->num_depths) return DAS_ERR_DEPTH;
+  const int kplane = c->k_plane[kappa];
+  const int vplane = c->v_plane[nu];
+  if (kplane < 0 || vplane < 0) return DAS_ERR_DEPTH;
+  Plan plan;
+  st = make_plan(c, b, hq, w, o, &plan);
+  if (st != DAS_OK) return st;
+  if (!ws || ws_bytes < plan.total) return DAS_ERR_WORKSPACE;
+  if (reinterpret_cast<uintptr_t>(ws) % kAlign != 0) return DAS_ERR_WORKSPACE;
+
+  const int dh = c->head_dim;
+  const size_t eb = static_cast<size_t>(elem_bytes(c->dtype));
+  const size_t layer_elems = static_cast<size_t>(c->num_kv_heads) * c->num_pages * kPage * dh;
+  AttnParams p;
+  p.k_layer = static_cast<const char *>(c->k_pool) +
+              (static_cast<size_t>(kplane) * c->num_layers + layer) * layer_elems * eb;
+  p.v_layer = static_cast<const char *>(c->v_pool) +
+              (static_cast<size_t>(vplane) * c->num_layers + layer) * layer_elems * eb;
+  p.q = q;
+  p.kb = kb;
+  p.vb = vb;
+  p.out = out;
+  p.lse = lse;
+  p.prefix_len = b->prefix_len;
+  p.block_table = b->block_table;
+  p.dev_error = b->dev_error;
+  char *wsb = static_cast<char *>(ws);
+  p.ws_o = reinterpret_cast<float *>(wsb);
+  p.ws_m = reinterpret_cast<float *>(wsb + plan.ws_o_bytes);
+  p.ws_l = reinterpret_cast<float *>(wsb + plan.ws_o_bytes + plan.ws_ml_bytes);
+  p.batch = b->batch;
+  p.hq = hq;
+  p.hkv = c->num_kv_heads;
+  p.group = hq / c->num_kv_heads;
+  p.w = w;
+  p.rows = plan.rows;
+  p.num_pages = c->num_pages;
+  p.max_pages = b->max_pages_per_seq;
+  p.pages_per_split = plan.pages_per_split;
+  p.nsplit = plan.nsplit;
+  // log2(e) / sqrt(dh): logits are kept in base-2 units so exp2 can be used.
+  const double log2e = 1.4426950408889634074;
+  p.scale_log2 = static_cast<float>(log2e / __builtin_sqrt(static_cast<double>(dh)));
+
+  hipError_t e = plan.path == DAS_PATH_MFMA ? launch_attn_mfma(p, dh, stream)
+                                            : launch_attn_valu(p, c->dtype, dh, stream);
+  if (e != hipSuccess) return DAS_ERR_HIP;
+  e = launch_attn_combine(p, c->dtype, dh, stream);
+  if (e != hipSuccess) return DAS_ERR_HIP;
+  return DAS_OK;
+}
+
+}  // namespace
+}  // namespace das
+
+using namespace das;
+
+extern "C" {
+
+size_t das_attn_workspace_bytes_ex(const das_cache *cache, const das_batch *batch,
+                                   int32_t num_q_heads, int32_t block_len,
+                                   const das_attn_options *opts) {
+  if (check_cache(cache) != DAS_OK || check_batch(batch) != DAS_OK) return 0;
+  Plan plan;
+  if (make_plan(cache, batch, num_q_heads, block_len, opts, &plan) != DAS_OK) return 0;
+  return plan.total;
+}
+
+size_t das_attn_workspace_bytes(const das_cache *cache, const das_batch *batch,
+                                int32_t num_q_heads, int32_t block_len) {
+  return das_attn_workspace_bytes_ex(cache, batch, num_q_heads, block_len, nullptr);
+}
+
+das_status das_attn_policy(const das_cache *cache, const das_batch *batch, int32_t layer,
+                           int32_t kappa, int32_t nu, int32_t num_q_heads, int32_t block_len,
+                           const void *q, const void *k_blk, const void *v_blk, void *out,
+                           float *lse, void *workspace, size_t workspace_bytes,
+                           const das_attn_options *opts, hipStream_t stream) {
+  return attn_common(cache, batch, layer, kappa, nu, num_q_heads, block_len, q, k_blk, v_blk,
+                     out, lse, workspace, workspace_bytes, opts, stream);
+}
+
+das_status das_attn_draft_maturev(const das_cache *cache, const das_batch *batch,
+                                  int32_t layer, int32_t draft_depth, int32_t num_q_heads,
+                                  int32_t block_len, const void *q, const void *k_blk,
+                                  const void *v_blk, void *out, float *lse, void *workspace,
+                                  size_t workspace_bytes, hipStream_t stream) {
+  if (!cache) return DAS_ERR_NULL;
+  // Mature-V: keys at the draft depth, values at the full depth R.
+  return attn_common(cache, batch, layer, draft_depth, cache->num_depths, num_q_heads,
+                     block_len, q, k_blk, v_blk, out, lse, workspace, workspace_bytes,
+                     nullptr, stream);
+}
+
+das_status das_attn_verify(const das_cache *cache, const das_batch *batch, int32_t layer,
+                           int32_t depth, int32_t num_q_heads, int32_t block_len,
+                           const void *q, const void *k_blk, const void *v_blk, void *out,
+                           float *lse, void *workspace, size_t workspace_bytes,
+                           hipStream_t stream) {
+  // Aligned read: keys and values at the same depth.
+  return attn_common(cache, batch, layer, depth, depth, num_q_heads, block_len, q, k_blk,
+                     v_blk, out, lse, workspace, workspace_bytes, nullptr, stream);
+}
+
+das_status das_kv_append(const das_cache *cache, const das_batch *batch, const void *k_new,
+                         const void *v_new, int32_t w_max, const int32_t *num_new,
+                         int32_t *len_out, hipStream_t stream) {
+  das_status st = check_cache(cache);
+  if (st != DAS_OK) return st;
+  st = check_batch(batch);
+  if (st != DAS_OK) return st;
+  if (!k_new || !v_new || !num_new) return DAS_ERR_NULL;
+  if (w_max < 1 || w_max > DAS_MAX_BLOCK) return DAS_ERR_SHAPE;
+  if (len_out && static_cast<const void *>(len_out) ==
+                     static_cast<const void *>(batch->prefix_len))
+    return DAS_ERR_SHAPE;
+  AppendParams p;
+  p.k_new = k_new;
+  p.v_new = v_new;
+  p.k_pool = cache->k_pool;
+  p.v_pool = cache->v_pool;
+  p.prefix_len = batch->prefix_len;
+  p.block_table = batch->block_table;
+  p.num_new = num_new;
+  p.len_out = len_out;
+  p.dev_error = batch->dev_error;
+  p.batch = batch->batch;
+  p.n_k_planes = cache->num_k_planes;
+  p.n_v_planes = cache->num_v_planes;
+  p.layers = cache->num_layers;
+  p.hkv = cache->num_kv_heads;
+  p.num_pages = cache->num_pages;
+  p.max_pages = batch->max_pages_per_seq;
+  p.w_max = w_max;
+  if (launch_kv_append(p, cache->dtype, cache->head_dim, stream) != hipSuccess)
+    return DAS_ERR_HIP;
+  return DAS_OK;
+}
+
+const char *das_status_string(das_status status) {
+  switch (status) {
+    case DAS_OK: return "ok";
+    case DAS_ERR_NULL: return "a required pointer is NULL";
+    case DAS_ERR_SHAPE: return "a size is out of range or inconsistent";
+    case DAS_ERR_DEPTH: return "depth outside 1..R or not stored in the cache";
+    case DAS_ERR_DTYPE: return "unknown element type";
+    case DAS_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
+    case DAS_ERR_HIP: return "a HIP kernel launch failed";
+    case DAS_ERR_UNSUPPORTED: return "request not supported by this build";
+  }
+  return "unknown status";
+}
+
+int32_t das_version(void) { return 100; }
+
+}  // extern "C"

@@ -1,0 +1,97 @@
+// Internal declarations shared by the host dispatcher and the kernels of the
+// DAS attention library. Not part of the public C ABI (include/das.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "das.h"
+
+namespace das {
+
+constexpr int kPage = DAS_PAGE_TOKENS;  // tokens per cache page
+
+// Everything one attention launch needs. Pointers are device pointers; the
+// pool pointers already include the plane and core-layer offsets, so a
+// kernel only adds (kv head, page) offsets.
+struct AttnParams {
+  const void *k_layer;   // [Hkv][P][64][dh]   keys of plane kappa, layer l
+  const void *v_layer;   // [Hkv][P][dh][64]   values of plane nu, layer l
+  const void *q;         // [B][w][Hq][dh]
+  const void *kb;        // [B][w][Hkv][dh]
+  const void *vb;        // [B][w][Hkv][dh]
+  void *out;             // [B][w][Hq][dh]
+  float *lse;            // [B][Hq][w] or nullptr
+  const int32_t *prefix_len;   // [B]
+  const int32_t *block_table;  // [B][max_pages]
+  uint32_t *dev_error;         // or nullptr
+  float *ws_o;           // [B][Hkv][nsplit][rows][dh]   unnormalised partial O
+  float *ws_m;           // [B][Hkv][nsplit][rows]       running max (log2 units)
+  float *ws_l;           // [B][Hkv][nsplit][rows]       running sum
+  int32_t batch, hq, hkv, group, w, rows;  // rows = w * group
+  int32_t num_pages, max_pages;
+  int32_t pages_per_split, nsplit;
+  float scale_log2;      // log2(e) / sqrt(dh): logits in base-2 units
+};
+
+struct AppendParams {
+  const void *k_new;     // [nK][L][B][w_max][Hkv][dh]
+  const void *v_new;     // [nV][L][B][w_max][Hkv][dh]
+  void *k_pool;          // [nK][L][Hkv][P][64][dh]
+  void *v_pool;          // [nV][L][Hkv][P][dh][64]
+  const int32_t *prefix_len;
+  const int32_t *block_table;
+  const int32_t *num_new;
+  int32_t *len_out;
+  uint32_t *dev_error;
+  int32_t batch, n_k_planes, n_v_planes, layers, hkv, num_pages, max_pages, w_max;
+};
+
+// Launchers (return the hipError_t of the launch).
+hipError_t launch_attn_valu(const AttnParams &p, int dtype, int dh, hipStream_t s);
+hipError_t launch_attn_mfma(const AttnParams &p, int dh, hipStream_t s);
+hipError_t launch_attn_combine(const AttnParams &p, int dtype, int dh, hipStream_t s);
+hipError_t launch_kv_append(const AppendParams &p, int dtype, int dh, hipStream_t s);
+
+// Rows of one workgroup of the vector-ALU kernel and of the matrix-core kernel.
+constexpr int kValuRows = 32;
+int mfma_rows_per_wg(int rows);
+
+// ---------------------------------------------------------------------------
+// Device helpers
+// ---------------------------------------------------------------------------
+typedef uint16_t bf16_t;  // raw bfloat16 bits
+
+__device__ __forceinline__ float bf16_to_f32(bf16_t v) {
+  return __uint_as_float(static_cast<uint32_t>(v) << 16);
+}
+
+// Round to nearest, ties to even; NaN stays NaN.
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<bf16_t>((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return static_cast<bf16_t>(u >> 16);
+}
+
+template <typename T> __device__ __forceinline__ float to_f32(T v);
+template <> __device__ __forceinline__ float to_f32<float>(float v) { return v; }
+template <> __device__ __forceinline__ float to_f32<bf16_t>(bf16_t v) { return bf16_to_f32(v); }
+
+template <typename T> __device__ __forceinline__ T from_f32(float v);
+template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }
+template <> __device__ __forceinline__ bf16_t from_f32<bf16_t>(float v) { return f32_to_bf16(v); }
+
+__device__ __forceinline__ void report_error(uint32_t *word, uint32_t bits) {
+  if (word) atomicOr(word, bits);
+}
+
+// Sequence prefix length, clamped to what the block table can address; an
+// out-of-range value is reported once per sequence by the caller's thread 0.
+__device__ __forceinline__ int clamp_prefix(int s, int max_pages, bool *bad) {
+  const int cap = max_pages * kPage;
+  *bad = (s < 0) || (s > cap);
+  return s < 0 ? 0 : (s > cap ? cap : s);
+}
+
+}  // namespace das

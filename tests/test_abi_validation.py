@@ -1,0 +1,174 @@
+"""Host-side validation of the C ABI: bad arguments are rejected with the
+documented status before any HIP call, so nothing is enqueued."""
+
+import ctypes
+import os
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+import torch  # noqa: E402
+
+# The calls below pass fake device pointers and rely on validation failing
+# first; on a host with a visible GPU a validation bug could launch a kernel
+# on them, so these checks run on GPU-less hosts only (device_count does not
+# initialise the GPU).
+if torch.cuda.device_count() > 0:
+    pytest.skip("host-validation checks run on GPU-less hosts", allow_module_level=True)
+
+lib_mod = pytest.importorskip("paper_2609_34538_amd._lib")
+from paper_2609_34538_amd._lib import (DasBatchC, DasCacheC, DasOptionsC, LIB, MAX_DEPTH)  # noqa: E402
+
+OK, NULL, SHAPE, DEPTH, DTYPE, WS, HIP, UNSUP = 0, -1, -2, -3, -4, -5, -6, -7
+FAKE = 0x100000  # never dereferenced: every call below fails validation first
+
+
+def make_cache(dtype=1, R=32, L=4, hkv=8, dh=128, pages=100, kd=(3, 32), vd=(32,)):
+    c = DasCacheC()
+    c.dtype, c.num_depths, c.num_layers, c.num_kv_heads = dtype, R, L, hkv
+    c.head_dim, c.num_pages = dh, pages
+    c.num_k_planes, c.num_v_planes = len(kd), len(vd)
+    for r in range(MAX_DEPTH + 1):
+        c.k_plane[r] = -1
+        c.v_plane[r] = -1
+    for i, d in enumerate(kd):
+        c.k_plane[d] = i
+    for i, d in enumerate(vd):
+        c.v_plane[d] = i
+    c.k_pool = FAKE
+    c.v_pool = FAKE
+    return c
+
+
+def make_batch(B=4, maxp=10):
+    b = DasBatchC()
+    b.batch, b.max_pages_per_seq = B, maxp
+    b.prefix_len, b.block_table, b.dev_error = FAKE, FAKE, None
+    return b
+
+
+def ws_bytes(c, b, hq=32, w=8, opts=None):
+    if opts is None:
+        return LIB.das_attn_workspace_bytes(ctypes.byref(c), ctypes.byref(b), hq, w)
+    return LIB.das_attn_workspace_bytes_ex(ctypes.byref(c), ctypes.byref(b), hq, w,
+                                           ctypes.byref(opts))
+
+
+_AUTO = object()
+
+
+def draft(c, b, layer=0, d=3, hq=32, w=8, q=FAKE, ws=_AUTO, nbytes=None, ptrs=FAKE):
+    if ws is _AUTO:
+        ws = FAKE
+    if nbytes is None:
+        nbytes = ws_bytes(c, b, hq, w)
+    return LIB.das_attn_draft_maturev(ctypes.byref(c), ctypes.byref(b), layer, d, hq, w, q,
+                                      ptrs, ptrs, ptrs, None, ws, nbytes, None)
+
+
+def test_workspace_size_formula():
+    c, b = make_cache(), make_batch()
+    n = ws_bytes(c, b)
+    assert n > 0 and n % 256 == 0
+    # grows with the number of rows and is zero for rejected shapes
+    assert ws_bytes(c, b, hq=32, w=16) > n
+    assert ws_bytes(c, b, hq=33) == 0
+    assert ws_bytes(c, b, w=0) == 0
+    assert ws_bytes(c, b, w=65) == 0
+    # explicit split size: nsplit = ceil(maxp / pps)
+    o = DasOptionsC()
+    o.path, o.pages_per_split = 1, 1
+    rows, hkv, B, maxp, dh = 8 * 4, 8, 4, 10, 128
+    per = B * hkv * maxp * rows
+    al = lambda x: (x + 255) // 256 * 256
+    assert ws_bytes(c, b, opts=o) == al(per * dh * 4) + 2 * al(per * 4)
+
+
+@pytest.mark.parametrize("field,value,code", [
+    ("dtype", 7, DTYPE), ("num_depths", 0, SHAPE), ("num_depths", MAX_DEPTH + 1, SHAPE),
+    ("num_layers", 0, SHAPE), ("num_kv_heads", 0, SHAPE), ("head_dim", 80, SHAPE),
+    ("num_pages", 0, SHAPE), ("num_k_planes", 0, SHAPE), ("k_pool", None, NULL),
+    ("v_pool", None, NULL),
+])
+def test_bad_cache_rejected(field, value, code):
+    c, b = make_cache(), make_batch()
+    nbytes = ws_bytes(c, b)
+    setattr(c, field, value)
+    assert draft(c, b, ws=FAKE, nbytes=nbytes) == code
+
+
+def test_bad_plane_map_rejected():
+    c, b = make_cache(), make_batch()
+    c.k_plane[5] = 7  # beyond num_k_planes
+    assert draft(c, b, ws=FAKE, nbytes=1 << 30) == SHAPE
+
+
+@pytest.mark.parametrize("field,value,code", [
+    ("batch", 0, SHAPE), ("max_pages_per_seq", 0, SHAPE), ("prefix_len", None, NULL),
+    ("block_table", None, NULL),
+])
+def test_bad_batch_rejected(field, value, code):
+    c, b = make_cache(), make_batch()
+    nbytes = ws_bytes(c, b)
+    setattr(b, field, value)
+    assert draft(c, b, ws=FAKE, nbytes=nbytes) == code
+
+
+def test_attention_argument_checks():
+    c, b = make_cache(), make_batch()
+    n = ws_bytes(c, b)
+    assert draft(c, b, q=None) == NULL
+    assert draft(c, b, ptrs=None) == NULL
+    assert draft(c, b, layer=4) == SHAPE
+    assert draft(c, b, layer=-1) == SHAPE
+    assert draft(c, b, d=0, ws=FAKE, nbytes=n) == DEPTH
+    assert draft(c, b, d=33, ws=FAKE, nbytes=n) == DEPTH
+    assert draft(c, b, d=2, ws=FAKE, nbytes=n) == DEPTH  # K at depth 2 not stored
+    assert draft(c, b, hq=36, ws=FAKE, nbytes=n) == SHAPE  # not a multiple of Hkv
+    assert draft(c, b, hq=80, ws=FAKE, nbytes=1 << 30) == UNSUP  # group of 10
+    assert draft(c, b, w=0, ws=FAKE, nbytes=n) == SHAPE
+    assert draft(c, b, w=65, ws=FAKE, nbytes=n) == SHAPE
+    assert draft(c, b, ws=None, nbytes=n) == WS
+    assert draft(c, b, ws=FAKE, nbytes=n - 1) == WS
+    assert draft(c, b, ws=FAKE + 4, nbytes=n) == WS  # not 256-byte aligned
+    # V at the full depth must be stored for a Mature-V read
+    c2 = make_cache(vd=(31,))
+    assert draft(c2, b, ws=FAKE, nbytes=n) == DEPTH
+
+
+def test_verify_and_policy_checks():
+    c, b = make_cache(), make_batch()
+    n = ws_bytes(c, b)
+    v = LIB.das_attn_verify(ctypes.byref(c), ctypes.byref(b), 0, 3, 32, 8, FAKE, FAKE, FAKE,
+                            FAKE, None, FAKE, n, None)
+    assert v == DEPTH  # V at depth 3 is not stored
+    o = DasOptionsC()
+    o.path, o.pages_per_split = 2, 0
+    f32 = make_cache(dtype=0)
+    assert LIB.das_attn_policy(ctypes.byref(f32), ctypes.byref(b), 0, 32, 32, 32, 8, FAKE, FAKE,
+                               FAKE, FAKE, None, FAKE, 1 << 30, ctypes.byref(o), None) == UNSUP
+    o.path = 9
+    assert LIB.das_attn_policy(ctypes.byref(c), ctypes.byref(b), 0, 32, 32, 32, 8, FAKE, FAKE,
+                               FAKE, FAKE, None, FAKE, 1 << 30, ctypes.byref(o), None) == SHAPE
+    o.path, o.pages_per_split = 0, -1
+    assert LIB.das_attn_policy(ctypes.byref(c), ctypes.byref(b), 0, 32, 32, 32, 8, FAKE, FAKE,
+                               FAKE, FAKE, None, FAKE, 1 << 30, ctypes.byref(o), None) == SHAPE
+
+
+def test_append_argument_checks():
+    c, b = make_cache(), make_batch()
+    app = lambda k=FAKE, v=FAKE, w=32, n=FAKE, lo=None, cc=c, bb=b: LIB.das_kv_append(
+        ctypes.byref(cc), ctypes.byref(bb), k, v, w, n, lo, None)
+    assert app(k=None) == NULL
+    assert app(v=None) == NULL
+    assert app(n=None) == NULL
+    assert app(w=0) == SHAPE
+    assert app(w=65) == SHAPE
+    assert app(lo=FAKE) == SHAPE  # len_out aliases prefix_len
+    bad = make_cache()
+    bad.head_dim = 100
+    assert app(cc=bad) == SHAPE
+    nb = make_batch()
+    nb.block_table = None
+    assert app(bb=nb) == NULL
