@@ -45,7 +45,7 @@ int choose_path(const das_cache *c, const das_attn_options *o) {
   const int want = o ? o->path : DAS_PATH_AUTO;
   if (c->dtype == DAS_F32) return DAS_PATH_VALU;
   if (want == DAS_PATH_VALU || want == DAS_PATH_MFMA) return want;
-  return DAS_PATH_VALU;
+  return DAS_PATH_MFMA;
 }
 
 struct Plan {
@@ -80,7 +80,9 @@ das_status make_plan(const das_cache *c, const das_batch *b, int hq, int w,
   if (pps == 0) {
     const long target_wgs = 2048;
     long want = (static_cast<long>(maxp) * units + target_wgs - 1) / target_wgs;
-    if (want < 2) want = 2;
+    // the matrix-core kernel spreads a split's pages over its 4 waves
+    const long min_pps = plan->path == DAS_PATH_MFMA ? 4 : 2;
+    if (want < min_pps) want = min_pps;
     pps = static_cast<int>(want);
   }
   if (pps > maxp) pps = maxp;
