@@ -138,7 +138,9 @@ typedef enum das_attn_path {
 
 typedef struct das_attn_options {
   int32_t path;             /* das_attn_path                                 */
-  int32_t pages_per_split;  /* prefix pages per workgroup; 0 = library choice */
+  int32_t pages_per_split;  /* prefix pages per workgroup; 0 = library choice;
+                               clamped to the block table width, and to 128
+                               on the matrix-core path                       */
 } das_attn_options;
 
 /*
@@ -164,7 +166,9 @@ size_t das_attn_workspace_bytes_ex(const das_cache *cache, const das_batch *batc
  *   out    [B][w][Hq][head_dim]   written, same dtype as the inputs
  *   lse    [B][Hq][w] fp32        optional natural-log softmax normaliser
  *   workspace                     >= das_attn_workspace_bytes(...) bytes,
- *                                 256-byte aligned, contents need no init
+ *                                 256-byte aligned, contents need no init;
+ *                                 calls that run concurrently need separate
+ *                                 workspaces
  *
  * w = block_len in 1..DAS_MAX_BLOCK; Hq a multiple of Hkv with Hq/Hkv <= 8;
  * layer in 0..L-1; draft_depth in 1..R; K at draft_depth and V at R stored.

@@ -86,6 +86,7 @@ das_status make_plan(const das_cache *c, const das_batch *b, int hq, int w,
     pps = static_cast<int>(want);
   }
   if (pps > maxp) pps = maxp;
+  if (plan->path == DAS_PATH_MFMA && pps > kMaxPagesPerSplit) pps = kMaxPagesPerSplit;
   plan->pages_per_split = pps;
   plan->nsplit = (maxp + pps - 1) / pps;
   const size_t per_split_rows =
@@ -150,11 +151,11 @@ das_status attn_common(const das_cache *c, const das_batch *b, int layer, int ka
   const double log2e = 1.4426950408889634074;
   p.scale_log2 = static_cast<float>(log2e / __builtin_sqrt(static_cast<double>(dh)));
 
-  hipError_t e = plan.path == DAS_PATH_MFMA ? launch_attn_mfma(p, dh, stream)
-                                            : launch_attn_valu(p, c->dtype, dh, stream);
+  const bool mfma = plan.path == DAS_PATH_MFMA;
+  const hipError_t e = mfma ? launch_attn_mfma(p, dh, stream)
+                            : launch_attn_valu(p, c->dtype, dh, stream);
   if (e != hipSuccess) return DAS_ERR_HIP;
-  e = launch_attn_combine(p, c->dtype, dh, stream);
-  if (e != hipSuccess) return DAS_ERR_HIP;
+  if (launch_attn_combine(p, c->dtype, dh, mfma ? 1 : 0, stream) != hipSuccess) return DAS_ERR_HIP;
   return DAS_OK;
 }
 

@@ -10,6 +10,7 @@
 namespace das {
 
 constexpr int kPage = DAS_PAGE_TOKENS;  // tokens per cache page
+constexpr int kMaxPagesPerSplit = 128;  // matrix-core kernel: page ids held one per lane
 
 // Everything one attention launch needs. Pointers are device pointers; the
 // pool pointers already include the plane and core-layer offsets, so a
@@ -50,7 +51,10 @@ struct AppendParams {
 // Launchers (return the hipError_t of the launch).
 hipError_t launch_attn_valu(const AttnParams &p, int dtype, int dh, hipStream_t s);
 hipError_t launch_attn_mfma(const AttnParams &p, int dh, hipStream_t s);
-hipError_t launch_attn_combine(const AttnParams &p, int dtype, int dh, hipStream_t s);
+// skip_single: sequences whose prefix fits one split were already written
+// by the attention kernel (matrix-core path).
+hipError_t launch_attn_combine(const AttnParams &p, int dtype, int dh, int skip_single,
+                               hipStream_t s);
 hipError_t launch_kv_append(const AppendParams &p, int dtype, int dh, hipStream_t s);
 
 // Rows of one workgroup of the vector-ALU kernel and of the matrix-core kernel.
