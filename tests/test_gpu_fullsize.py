@@ -1,0 +1,112 @@
+"""Parity at the full workload sizes, in the launch configuration bench.py
+times (library-chosen kernel path and split size), on sampled sequences that
+the fp64 oracle recomputes one by one."""
+
+from __future__ import annotations
+
+import gc
+
+import numpy as np
+import pytest
+import torch
+
+from gpu_common import assert_close, oracle_call, wrap
+from paper_2609_34538_amd import _lib as das
+from paper_2609_34538_amd import datagen as dg
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+W = dg.WORKLOADS
+
+
+@pytest.fixture(autouse=True)
+def _release_memory():
+    yield
+    gc.collect()
+    torch.cuda.empty_cache()
+
+
+def _check_rounds(cd, layer, seqs, rounds):
+    wl = cd.wl
+    cache, batch = wrap(cd)
+    R = wl.depth_R
+    for d, w in rounds:
+        q, kb, vb = dg.block_inputs(cd, w, d, DEV)
+        lse = torch.empty((wl.batch, wl.hq, w), dtype=torch.float32, device=DEV)
+        out = das.attn_draft_maturev(cache, batch, layer, d, q, kb, vb, lse=lse)
+        torch.cuda.synchronize()
+        ref, ref_lse = oracle_call(cd, layer, d, R, q, kb, vb, seqs)
+        assert_close(out[seqs], ref, wl.dtype, f"{wl.name} draft d={d} w={w} layer={layer}")
+        np.testing.assert_allclose(lse[seqs].double().cpu().numpy(), ref_lse, atol=1e-3)
+    q, kb, vb = dg.block_inputs(cd, wl.verify_width, R, DEV)
+    out = das.attn_verify(cache, batch, layer, R, q, kb, vb)
+    torch.cuda.synchronize()
+    ref, _ = oracle_call(cd, layer, R, R, q, kb, vb, seqs)
+    assert_close(out[seqs], ref, wl.dtype, f"{wl.name} verify layer={layer}")
+
+
+def test_config1_tiny_fp32_full():
+    cd = dg.make_cache(W[1], DEV)
+    _check_rounds(cd, 0, [0], [(1, 4)])
+
+
+def test_config2_single_sequence_full():
+    wl = W[2]
+    cd = dg.make_cache(wl, DEV)
+    assert cd.k_pool.shape[0] == 32 and cd.v_pool.shape[0] == 32  # every depth stored
+    for layer in (0, 3):
+        _check_rounds(cd, layer, [0], [(4, 8)])
+
+
+def test_config3_ragged_paged_full():
+    wl = W[3]
+    cd = dg.make_cache(wl, DEV)
+    assert cd.prefix_lens.min() >= 512 and cd.prefix_lens.max() <= 4096
+    _check_rounds(cd, 2, list(range(wl.batch)), [(2, 16)])
+
+
+def test_config4_long_prefix_gqa_full():
+    wl = W[4]
+    cd = dg.make_cache(wl, DEV)
+    cache, batch = wrap(cd)
+    # the workload's logits have standard deviation ~3 at the draft depth
+    q, kb, vb = dg.block_inputs(cd, 32, 3, DEV)
+    kc = dg.gather_prefix_k(cd, 0, cd.k_plane[3], 1, 4096)
+    q0 = q[0].double().cpu().numpy()
+    logits = np.einsum("wgd,sd->wgs", q0[:, :wl.group], kc[:, 0]) / np.sqrt(128)
+    assert 2.7 <= logits.std() <= 3.3, logits.std()
+    _check_rounds(cd, 1, [0, 3], [(3, 32)])
+
+
+def test_config5_das_wave_step_full():
+    """Draft rounds at d = 1..4 over blocks of 4, 8, 16, 32, the verifier over
+    32, the commit of U{0..32} accepted tokens per sequence, and a draft that
+    reads the grown prefix."""
+    wl = W[5]
+    cd = dg.make_cache(wl, DEV)
+    seqs = [0, 17]
+    rounds = list(zip(wl.draft_depths, wl.draft_widths))
+    _check_rounds(cd, 3, seqs, rounds)
+    cache, batch = wrap(cd)
+    k_new, v_new, num_new = dg.commit_inputs(cd, 32, DEV)
+    len_out = torch.empty(wl.batch, dtype=torch.int32, device=DEV)
+    das.kv_append(cache, batch, k_new, v_new, torch.as_tensor(num_new, device=DEV), len_out)
+    torch.cuda.synchronize()
+    new_lens = cd.prefix_lens + num_new
+    assert len_out.cpu().numpy().tolist() == new_lens.tolist()
+    for b in seqs + [5, 31]:
+        s, n = int(cd.prefix_lens[b]), int(num_new[b])
+        for layer in (0, 3):
+            for r, pl in cd.k_plane.items():
+                got = dg.gather_prefix_k(cd, b, pl, layer, s + n)[s:]
+                np.testing.assert_array_equal(got, k_new[pl, layer, b, :n].double().cpu().numpy())
+            for r, pl in cd.v_plane.items():
+                got = dg.gather_prefix_v(cd, b, pl, layer, s + n)[s:]
+                np.testing.assert_array_equal(got, v_new[pl, layer, b, :n].double().cpu().numpy())
+    # next block reads the committed prefix
+    _, batch2 = wrap(cd, prefix_lens=new_lens)
+    q, kb, vb = dg.block_inputs(cd, 4, 1, DEV)
+    out = das.attn_draft_maturev(cache, batch2, 3, 1, q, kb, vb)
+    torch.cuda.synchronize()
+    ref, _ = oracle_call(cd, 3, 1, wl.depth_R, q, kb, vb, seqs, prefix_lens=new_lens)
+    assert_close(out[seqs], ref, wl.dtype, "draft after commit")
