@@ -139,7 +139,7 @@ typedef enum das_attn_path {
 typedef struct das_attn_options {
   int32_t path;             /* das_attn_path                                 */
   int32_t pages_per_split;  /* prefix pages per workgroup; 0 = library choice;
-                               clamped to the block table width, and to 128
+                               clamped to the block table width, and to 64
                                on the matrix-core path                       */
 } das_attn_options;
 

@@ -18,7 +18,8 @@ from typing import Dict, Optional
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libdas.so")
+# DAS_LIBRARY may point at another build of the same library.
+LIB_PATH = os.environ.get("DAS_LIBRARY") or os.path.join(_HERE, "libdas.so")
 
 MAX_DEPTH = 64
 PAGE_TOKENS = 64

@@ -1,13 +1,22 @@
 // Matrix-core (MFMA) policy-attention kernel for bf16 caches (Eq. (2)-(3)).
 //
-// One workgroup = 4 waves on one (sequence, KV head, prefix split, row tile).
-// The split's tiles are its 64-token prefix pages, plus the draft block on
-// split 0; wave w takes tiles w, w+4, ... and keeps a private online-softmax
-// state, with the next tile's key/value fragments loaded into registers while
-// the current one is computed. The four states are merged through LDS.
-// A sequence whose prefix fits one split is normalised and written out
-// here; otherwise each split leaves its partial (O, m, l) in the workspace
-// for the combine kernel.
+// Persistent one-wave workers. The work of a call is cut into chunks =
+// (sequence, KV head, row tile of 16 * NQ query rows, prefix split of up to
+// pages_per_split pages); split 0 of every (sequence, head, row tile) also
+// carries the draft block. Chunks are enumerated with every full split first
+// and the shorter last splits after them, and worker r (ranked XCD-major)
+// takes chunks r, r + W, r + 2W, ... (W = number of workers): every worker
+// gets about the same number of full chunks, and consecutive chunks (the row
+// tiles of one split) land on the same XCD and share its L2.
+//
+// Each worker streams the half pages (32 tokens) of its chunks, one chunk
+// after the other, through a private ring of NB LDS slots filled by the
+// direct-to-LDS loads of gfx950 (global_load_lds_dwordx4), up to NB tiles
+// ahead of the tile being computed and across chunk boundaries; each chunk's
+// Q fragments are loaded into one of two LDS buffers the same way when the
+// stream enters the chunk. The worker waits on its own vector-memory counter
+// for the data it reads. Chunk descriptors and page ids are decoded into LDS
+// a batch of chunks at a time.
 //
 // Both products run on v_mfma_f32_16x16x32_bf16 with the key/value tile as
 // the A operand, so softmax probabilities never leave registers:
@@ -22,8 +31,10 @@
 // of the P^T fragment of the P.V product, and the matching V^T fragment is
 // one contiguous 16-byte load from the dim-major value page.
 //
-// Query rows of a row tile: row = i * G + g (block position i, head
-// kvh * G + g). Logits are scaled into base-2 units after the product.
+// A chunk ends by writing its (m, l, O) partial to the workspace for the
+// combine kernel, or, when its sequence has a single split, the normalised
+// output. Query rows of a row tile: row = i * G + g (block position i,
+// head kvh * G + g). Logits are scaled into base-2 units after the product.
 
 #include "das_internal.h"
 
@@ -33,12 +44,39 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
 
 constexpr float kNegInf = -__builtin_huge_valf();
+constexpr int kFragBytes = 64 * 16;  // one 16-byte fragment per lane
+constexpr int kBatch = 8;            // chunk descriptors decoded at a time
+constexpr int kMaxSeqBlocks = 64;    // sequences are scanned 64 at a time
 
 __device__ __forceinline__ u32x4 load16(const bf16_t *ptr) {
   return *reinterpret_cast<const u32x4 *>(ptr);
+}
+
+// 16 bytes per lane, global -> LDS at lds + 16 * lane (lds wave-uniform).
+__device__ __forceinline__ void dma16(const bf16_t *src, uint8_t *lds) {
+  __builtin_amdgcn_global_load_lds((__attribute__((address_space(1))) void *)(src),
+                                   (__attribute__((address_space(3))) void *)(lds), 16, 0, 0);
+}
+
+// s_waitcnt vmcnt(n), other counters untouched (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// Wait until at most `tiles` page tiles of NF loads each are outstanding.
+// Any other loads issued later only make the wait stricter.
+template <int NF>
+__device__ __forceinline__ void wait_tiles(int tiles) {
+  if (tiles <= 0) wait_vmcnt<0>();
+  else if (tiles == 1) wait_vmcnt<NF>();
+  else if (tiles == 2) wait_vmcnt<(2 * NF < 64 ? 2 * NF : 0)>();
+  else wait_vmcnt<(3 * NF < 64 ? 3 * NF : 0)>();
 }
 
 __device__ __forceinline__ f32x4 mfma16x16x32(u32x4 a, u32x4 b, f32x4 c) {
@@ -51,48 +89,17 @@ __device__ __forceinline__ int slot_token(int tt, int m) {
   return 32 * (tt >> 1) + 8 * (m >> 2) + 4 * (tt & 1) + (m & 3);
 }
 
-// Key/value fragments of one half page (32 tokens, S^T tiles 2u and 2u+1).
-template <int DH>
-struct Frags {
-  u32x4 k[2][DH / 32];
-  u32x4 v[DH / 16];
+template <int DH, int NQ, int NB_>
+struct Geo {
+  static constexpr int KS = DH / 32;       // k steps of Q K^T
+  static constexpr int DT = DH / 16;       // head-dim tiles of P V
+  static constexpr int NF = 2 * KS + DT;   // fragments (loads) per half-page tile
+  static constexpr int SLOT = NF * kFragBytes;
+  static constexpr int NB = NB_;           // ring depth
+  static constexpr int QF = NQ * KS;       // Q fragments of a row tile
+  static constexpr int LDS = NB * SLOT + 2 * QF * kFragBytes + kBatch * (8 + 64) * 4 +
+                             2 * kMaxSeqBlocks * 4;
 };
-
-template <int DH>
-__device__ __forceinline__ void load_half(Frags<DH> &f, const bf16_t *kp, const bf16_t *vp,
-                                          int u, int ln, int lg) {
-#pragma unroll
-  for (int e = 0; e < 2; ++e) {
-    const int tok = slot_token(2 * u + e, ln);
-#pragma unroll
-    for (int ks = 0; ks < DH / 32; ++ks) f.k[e][ks] = load16(kp + tok * DH + 32 * ks + 8 * lg);
-  }
-#pragma unroll
-  for (int dt = 0; dt < DH / 16; ++dt) f.v[dt] = load16(vp + (16 * dt + ln) * kPage + 32 * u + 8 * lg);
-}
-
-// Draft block half u: token-major K/V of stride Hkv * DH, w <= 64 tokens.
-template <int DH>
-__device__ __forceinline__ void load_block_half(Frags<DH> &f, const bf16_t *kb, const bf16_t *vb,
-                                                int u, int w, size_t tok_stride, int ln, int lg) {
-#pragma unroll
-  for (int e = 0; e < 2; ++e) {
-    const int tok = slot_token(2 * u + e, ln);
-#pragma unroll
-    for (int ks = 0; ks < DH / 32; ++ks)
-      f.k[e][ks] = tok < w ? load16(kb + tok * tok_stride + 32 * ks + 8 * lg) : u32x4{0, 0, 0, 0};
-  }
-#pragma unroll
-  for (int dt = 0; dt < DH / 16; ++dt) {
-    u16x8 v8;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int tok = 32 * u + 8 * lg + j;
-      v8[j] = tok < w ? vb[tok * tok_stride + 16 * dt + ln] : static_cast<uint16_t>(0);
-    }
-    f.v[dt] = __builtin_bit_cast(u32x4, v8);
-  }
-}
 
 template <int DH, int NQ>
 struct State {
@@ -100,14 +107,23 @@ struct State {
   f32x4 o[NQ][DH / 16];
 };
 
-// One half page through both products and the online softmax. Token t of
-// the half (0..31, page token 32u + t) is visible when t < limit for a
-// prefix page, and when t < w - 32u and 32u + t <= i for the draft block.
+// Key (2 x KS) and value (DT) fragments of one 32-token tile.
+template <int DH>
+struct Frags {
+  u32x4 k[2][DH / 32];
+  u32x4 v[DH / 16];
+};
+
+// One 32-token tile through both products and the online softmax. Token t of
+// the tile (0..31) is visible when t < limit and t <= cap (cap = i - 32u for
+// the draft block's half u, unbounded for prefix pages).
 template <int DH, int NQ>
-__device__ __forceinline__ void compute_half(State<DH, NQ> &st, const Frags<DH> &f,
+__device__ __forceinline__ void compute_tile(State<DH, NQ> &st, const Frags<DH> &f,
                                              const u32x4 (&qf)[NQ][DH / 32],
-                                             const int (&row_i)[NQ], bool blk, int u, int limit,
-                                             float scale, int lg) {
+                                             const int (&cap)[NQ], int limit, float scale,
+                                             int lg) {
+  u16x8 pf[NQ];
+  float alpha[NQ];
 #pragma unroll
   for (int qt = 0; qt < NQ; ++qt) {
     f32x4 sacc[2];
@@ -124,7 +140,7 @@ __device__ __forceinline__ void compute_half(State<DH, NQ> &st, const Frags<DH> 
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
         const int t = 8 * lg + 4 * e + v;
-        const bool vis = blk ? (t < limit && 32 * u + t <= row_i[qt]) : (t < limit);
+        const bool vis = (t < limit) & (t <= cap[qt]);
         x[e][v] = vis ? sacc[e][v] * scale : kNegInf;
         mx = fmaxf(mx, x[e][v]);
       }
@@ -133,233 +149,388 @@ __device__ __forceinline__ void compute_half(State<DH, NQ> &st, const Frags<DH> 
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
     const float mnew = fmaxf(st.m[qt], mx);
     const float muse = mnew == kNegInf ? 0.f : mnew;
-    const float alpha = exp2f(st.m[qt] - muse);
+    alpha[qt] = exp2f(st.m[qt] - muse);
     float psum = 0.f;
-    u16x8 pf;
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
         const __bf16 pb = static_cast<__bf16>(exp2f(x[e][v] - muse));
         psum += static_cast<float>(pb);
-        pf[4 * e + v] = __builtin_bit_cast(uint16_t, pb);
+        pf[qt][4 * e + v] = __builtin_bit_cast(uint16_t, pb);
       }
     }
     psum += __shfl_xor(psum, 16, 64);
     psum += __shfl_xor(psum, 32, 64);
-    st.l[qt] = st.l[qt] * alpha + psum;
+    st.l[qt] = st.l[qt] * alpha[qt] + psum;
     st.m[qt] = mnew;
+  }
 #pragma unroll
-    for (int dt = 0; dt < DH / 16; ++dt)
-      st.o[qt][dt] = mfma16x16x32(f.v[dt], __builtin_bit_cast(u32x4, pf), st.o[qt][dt] * alpha);
+  for (int dt = 0; dt < DH / 16; ++dt) {
+#pragma unroll
+    for (int qt = 0; qt < NQ; ++qt)
+      st.o[qt][dt] = mfma16x16x32(f.v[dt], __builtin_bit_cast(u32x4, pf[qt]), st.o[qt][dt] * alpha[qt]);
   }
 }
 
-template <int DH, int NQ>
-__global__ __launch_bounds__(256) void attn_mfma_kernel(AttnParams p, int n_rt, int n_items) {
-  constexpr int KS = DH / 32;
-  constexpr int DT = DH / 16;
-  constexpr int ROWS = 16 * NQ;
-  constexpr int OS = DH + 1;    // padded LDS row stride of the merge buffer
-  __shared__ float s_o[4][ROWS * OS];
-  __shared__ float s_m[4][ROWS];
-  __shared__ float s_l[4][ROWS];
+// Chunk counts of one block of 64 sequences (lane j holds sequence 64k + j).
+struct SeqBlock {
+  int k;            // block index held (-1: none)
+  int S;            // this lane's clamped prefix length
+  int npages;
+  int nfull;        // full splits x units
+  int npart;        // (1 if the last split is shorter or the prefix is empty) x units
+  int inclF, inclP; // inclusive prefix sums over the block's lanes
+};
 
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+template <int DH, int NQ, int NB>
+__global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, int n_workers) {
+  using G = Geo<DH, NQ, NB>;
+  constexpr int KS = G::KS;
+  constexpr int DT = G::DT;
+  constexpr int NF = G::NF;
+  constexpr int ROWS = 16 * NQ;
+  __shared__ __attribute__((aligned(16))) uint8_t ring[NB * G::SLOT];
+  __shared__ __attribute__((aligned(16))) uint8_t qbuf[2][G::QF * kFragBytes];
+  __shared__ int desc[kBatch][8];      // b, kvh, rt, split, pg0, npg, S, nsplit_b
+  __shared__ int pid[kBatch][64];      // page ids of each chunk
+  __shared__ int blkF[kMaxSeqBlocks];  // full-split chunks of each sequence block
+  __shared__ int blkP[kMaxSeqBlocks];  // last-split chunks of each sequence block
+
+  const int lane = threadIdx.x;
   const int ln = lane & 15;
   const int lg = lane >> 4;
-
-  // Workgroups are dealt to the 8 XCDs round-robin by linear id; the n_rt
-  // row tiles of one (sequence, head, split) get ids 8 apart, so they run on
-  // the same XCD and share its L2 for the key/value pages they all read.
-  const int lin = blockIdx.x;
-  const int rt = (lin >> 3) % n_rt;
-  const int item = ((lin >> 3) / n_rt) * 8 + (lin & 7);
-  if (item >= n_items) return;
-  const int split = item % p.nsplit;
-  const int unit = item / p.nsplit;
-  const int kvh = unit % p.hkv;
-  const int b = unit / p.hkv;
+  // worker rank, XCD-major: workgroups are dealt to the 8 XCDs round-robin
+  const int rank = (blockIdx.x & 7) * (n_workers >> 3) + (blockIdx.x >> 3);
   const int pps = p.pages_per_split;
-  const int pg0 = split * pps;
+  const int units = p.hkv * n_rt;  // chunks per split of one sequence
+  const int nblocks = (p.batch + 63) >> 6;
 
-  // Independent loads first: prefix length, the page ids of this wave's
-  // half-page tiles (wave w takes tiles w, w+4, ...; tile t is half t&1 of
-  // page t>>1, so lane j holds the id of split page w/2 + 2j), and Q.
-  const int s_raw = p.prefix_len[b];
-  int my_page = 0;
-  {
-    const int pi = (wave >> 1) + 2 * lane;
-    if (pi < pps && pg0 + pi < p.max_pages)
-      my_page = p.block_table[static_cast<size_t>(b) * p.max_pages + pg0 + pi];
-  }
-  const int row_base = rt * ROWS;
-  const bf16_t *q = static_cast<const bf16_t *>(p.q);
-  u32x4 qf[NQ][KS];
-  int row_i[NQ];
+  SeqBlock sb;
+  sb.k = -1;
+  auto load_block = [&](int k) {
+    const int b = 64 * k + lane;
+    const bool live = b < p.batch;
+    const int s_raw = live ? p.prefix_len[b] : 0;
+    bool bad;
+    const int S = clamp_prefix(s_raw, p.max_pages, &bad);
+    if (bad && live && rank == 0) report_error(p.dev_error, DAS_DEVERR_PREFIX);
+    sb.k = k;
+    sb.S = S;
+    sb.npages = (S + kPage - 1) / kPage;
+    sb.nfull = live ? (sb.npages / pps) * units : 0;
+    sb.npart = live ? ((sb.npages % pps) != 0 || sb.npages == 0 ? units : 0) : 0;
+    int f = sb.nfull, q = sb.npart;
 #pragma unroll
-  for (int qt = 0; qt < NQ; ++qt) {
-    const int row = row_base + qt * 16 + ln;
-    row_i[qt] = row / p.group;
-    if (row < p.rows) {
-      const int i = row / p.group, g = row % p.group;
-      const bf16_t *qrow = q + ((static_cast<size_t>(b) * p.w + i) * p.hq + kvh * p.group + g) * DH;
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) qf[qt][ks] = load16(qrow + 32 * ks + 8 * lg);
-    } else {
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) qf[qt][ks] = u32x4{0, 0, 0, 0};
+    for (int o = 1; o < 64; o <<= 1) {
+      const int fu = __shfl_up(f, o, 64), qu = __shfl_up(q, o, 64);
+      if (lane >= o) {
+        f += fu;
+        q += qu;
+      }
     }
-  }
+    sb.inclF = f;
+    sb.inclP = q;
+  };
 
-  bool bad_len;
-  const int S = clamp_prefix(s_raw, p.max_pages, &bad_len);
-  if (bad_len && split == 0 && kvh == 0 && rt == 0 && tid == 0)
-    report_error(p.dev_error, DAS_DEVERR_PREFIX);
-  const int npages = (S + kPage - 1) / kPage;
-  const int n_pg = max(0, min(pps, npages - pg0));  // prefix pages of this split
-  if (split > 0 && n_pg == 0) return;
-  // half-page tiles: 2 per prefix page, then the block's halves on split 0
-  const int ntiles = 2 * n_pg + (split == 0 ? (p.w + 31) / 32 : 0);
-  int nsplit_b = (npages + pps - 1) / pps;
-  if (nsplit_b < 1) nsplit_b = 1;
+  int totF = 0, totP = 0;
+  for (int k = 0; k < nblocks; ++k) {
+    load_block(k);
+    const int bf = __shfl(sb.inclF, 63, 64), bp = __shfl(sb.inclP, 63, 64);
+    if (lane == 0) {
+      blkF[k] = bf;
+      blkP[k] = bp;
+    }
+    totF += bf;
+    totP += bp;
+  }
+  const int total = totF + totP;
+  const int my_chunks = rank < total ? (total - rank + n_workers - 1) / n_workers : 0;
+  if (my_chunks == 0) return;
+
+  // Decode a batch of chunks into desc[] and pid[].
+  auto decode_batch = [&](int first, int count) {
+    int pages[kBatch];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      pages[j] = 0;
+      if (j >= count) continue;
+      const int c = rank + (first + j) * n_workers;
+      const bool phase2 = c >= totF;
+      int rem = phase2 ? c - totF : c;
+      int k = 0;
+      while (k < nblocks - 1) {
+        const int n = phase2 ? blkP[k] : blkF[k];
+        if (rem < n) break;
+        rem -= n;
+        ++k;
+      }
+      if (sb.k != k) load_block(k);
+      const int incl = phase2 ? sb.inclP : sb.inclF;
+      const int own = phase2 ? sb.npart : sb.nfull;
+      const unsigned long long m = __ballot(incl > rem);
+      const int lb = __builtin_ctzll(m);
+      const int local = rem - (__shfl(incl, lb, 64) - __shfl(own, lb, 64));
+      const int b = 64 * k + lb;
+      const int S = __shfl(sb.S, lb, 64);
+      const int npages = __shfl(sb.npages, lb, 64);
+      const int full = npages / pps;
+      const int nsb = max(1, (npages + pps - 1) / pps);
+      const int split = phase2 ? full : local / units;
+      const int u = local % units;
+      const int pg0 = split * pps;
+      const int npg = max(0, min(pps, npages - pg0));
+      if (lane == 0) {
+        desc[j][0] = b;
+        desc[j][1] = u / n_rt;
+        desc[j][2] = u % n_rt;
+        desc[j][3] = split;
+        desc[j][4] = pg0;
+        desc[j][5] = npg;
+        desc[j][6] = S;
+        desc[j][7] = nsb;
+      }
+      if (lane < npg) pages[j] = p.block_table[static_cast<size_t>(b) * p.max_pages + pg0 + lane];
+    }
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j)
+      if (j < count) pid[j][lane] = pages[j];
+  };
 
   const bf16_t *kl = static_cast<const bf16_t *>(p.k_layer);
   const bf16_t *vl = static_cast<const bf16_t *>(p.v_layer);
-  const size_t head_off = static_cast<size_t>(kvh) * p.num_pages * kPage * DH;
-  const bf16_t *kb = static_cast<const bf16_t *>(p.kb) +
-                     (static_cast<size_t>(b) * p.w * p.hkv + kvh) * DH;
-  const bf16_t *vb = static_cast<const bf16_t *>(p.vb) +
-                     (static_cast<size_t>(b) * p.w * p.hkv + kvh) * DH;
+  const size_t head_elems = static_cast<size_t>(p.num_pages) * kPage * DH;
   const size_t tok_stride = static_cast<size_t>(p.hkv) * DH;
 
-  State<DH, NQ> st;
-#pragma unroll
-  for (int qt = 0; qt < NQ; ++qt) {
-    st.m[qt] = kNegInf;
-    st.l[qt] = 0.f;
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) st.o[qt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  }
+  // Issue cursor: chunk ij of the batch (entered: its Q is loading), next
+  // half-page tile it; n_issued page tiles so far. Compute cursor: chunk cj,
+  // n_done page tiles consumed. Q of batch chunk j sits in qbuf[j & 1].
+  int batch_base = 0, batch_len = 0;
+  int ij = -1, it = 0, n_issued = 0;
+  int cj = 0, n_done = 0;
+  int q_tiles_before[2] = {0, 0};  // n_issued when each Q buffer was loaded
 
-  // Tile t: half t&1 of prefix page t>>1 (t < 2 n_pg), else half
-  // t - 2 n_pg of the block. Returns the visible-token limit of the half.
-  auto issue = [&](Frags<DH> &f, int t) -> int {
-    if (t < 2 * n_pg) {
-      const int page = __builtin_amdgcn_readlane(my_page, (t - wave) >> 2);
-      const bool ok = page >= 0 && page < p.num_pages;
-      if (!ok && lane == 0) report_error(p.dev_error, DAS_DEVERR_PAGE);
-      const size_t off = head_off + static_cast<size_t>(ok ? page : 0) * kPage * DH;
-      load_half<DH>(f, kl + off, vl + off, t & 1, ln, lg);
-      return ok ? min(32, S - (pg0 + (t >> 1)) * kPage - 32 * (t & 1)) : 0;
+  auto issue_q = [&](int j) {
+    const int b = desc[j][0], kvh = desc[j][1], rt = desc[j][2];
+    uint8_t *qb = qbuf[j & 1];
+#pragma unroll
+    for (int qt = 0; qt < NQ; ++qt) {
+      // rows past the last are clamped; their outputs are never written
+      const int row = min(rt * ROWS + qt * 16 + ln, p.rows - 1);
+      const int i = row / p.group, g = row % p.group;
+      const bf16_t *qrow = static_cast<const bf16_t *>(p.q) +
+                           ((static_cast<size_t>(b) * p.w + i) * p.hq + kvh * p.group + g) * DH;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) dma16(qrow + 32 * ks + 8 * lg, qb + (qt * KS + ks) * kFragBytes);
     }
-    const int u = t - 2 * n_pg;
-    load_block_half<DH>(f, kb, vb, u, p.w, tok_stride, ln, lg);
-    return p.w - 32 * u;
+    q_tiles_before[j & 1] = n_issued;
   };
 
-  Frags<DH> fa, fb;
-  int t = wave;
-  int lim_a = 0, lim_b = 0;
-  if (t < ntiles) lim_a = issue(fa, t);
-  while (t < ntiles) {
-    if (t + 4 < ntiles) lim_b = issue(fb, t + 4);
-    {
-      const bool blk = t >= 2 * n_pg;
-      compute_half<DH, NQ>(st, fa, qf, row_i, blk, blk ? t - 2 * n_pg : (t & 1), lim_a,
-                           p.scale_log2, lg);
-    }
-    t += 4;
-    if (t >= ntiles) break;
-    if (t + 4 < ntiles) lim_a = issue(fa, t + 4);
-    {
-      const bool blk = t >= 2 * n_pg;
-      compute_half<DH, NQ>(st, fb, qf, row_i, blk, blk ? t - 2 * n_pg : (t & 1), lim_b,
-                           p.scale_log2, lg);
-    }
-    t += 4;
-  }
-
-  // Merge the four waves (each lane holds head dims 16dt+4g.. of row n).
+  // Put one more page tile in the ring if there is room, entering the next
+  // chunk when the current one is exhausted (at most one chunk ahead of the
+  // compute cursor, so both Q buffers stay valid).
+  auto try_issue = [&]() {
+    while (true) {
+      if (ij >= 0 && it < 2 * desc[ij][5]) {
+        if (n_issued - n_done >= NB) return;
+        const int kvh = desc[ij][1];
+        const int page = pid[ij][it >> 1];
+        const bool ok = page >= 0 && page < p.num_pages;
+        if (!ok) report_error(p.dev_error, DAS_DEVERR_PAGE);
+        const size_t off = kvh * head_elems + static_cast<size_t>(ok ? page : 0) * kPage * DH;
+        uint8_t *slot = ring + (n_issued % NB) * G::SLOT;
+        const int u = it & 1;
 #pragma unroll
-  for (int qt = 0; qt < NQ; ++qt) {
-    const int r = qt * 16 + ln;
-    if (lg == 0) {
-      s_m[wave][r] = st.m[qt];
-      s_l[wave][r] = st.l[qt];
-    }
+        for (int e = 0; e < 2; ++e) {
+          const int tok = slot_token(2 * u + e, ln);
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt) {
+          for (int ks = 0; ks < KS; ++ks)
+            dma16(kl + off + tok * DH + 32 * ks + 8 * lg, slot + (e * KS + ks) * kFragBytes);
+        }
 #pragma unroll
-      for (int v = 0; v < 4; ++v) s_o[wave][r * OS + 16 * dt + 4 * lg + v] = st.o[qt][dt][v];
-    }
-  }
-  __syncthreads();
-
-  bf16_t *out = static_cast<bf16_t *>(p.out);
-  const int nrows = min(ROWS, p.rows - row_base);
-  if (nsplit_b == 1) {
-    // the whole prefix was this workgroup's: normalise and write the output
-    for (int e = tid; e < nrows * DH; e += 256) {
-      const int r = e / DH, c = e % DH;
-      float mx = fmaxf(fmaxf(s_m[0][r], s_m[1][r]), fmaxf(s_m[2][r], s_m[3][r]));
-      float o = 0.f, den = 0.f;
-#pragma unroll
-      for (int w4 = 0; w4 < 4; ++w4) {
-        const float sc = exp2f(s_m[w4][r] - mx);
-        o += sc * s_o[w4][r * OS + c];
-        den += sc * s_l[w4][r];
+        for (int dt = 0; dt < DT; ++dt)
+          dma16(vl + off + (16 * dt + ln) * kPage + 32 * u + 8 * lg, slot + (2 * KS + dt) * kFragBytes);
+        ++n_issued;
+        ++it;
+        return;
       }
-      const int row = row_base + r;
-      const int i = row / p.group, h = kvh * p.group + row % p.group;
-      out[((static_cast<size_t>(b) * p.w + i) * p.hq + h) * DH + c] = f32_to_bf16(o / den);
-      if (c == 0 && p.lse)
-        p.lse[(static_cast<size_t>(b) * p.hq + h) * p.w + i] = (mx + log2f(den)) * 0.69314718055994530942f;
+      const int nj = ij + 1;
+      if (nj >= batch_len || nj > cj + 1) return;
+      ij = nj;
+      it = 0;
+      issue_q(nj);
     }
-    return;
-  }
+  };
 
-  // Partial of this split to the workspace.
-  const size_t prow0 = ((static_cast<size_t>(b) * p.hkv + kvh) * p.nsplit + split) * p.rows + row_base;
-  for (int e = tid; e < nrows * DH; e += 256) {
-    const int r = e / DH, c = e % DH;
-    float mx = fmaxf(fmaxf(s_m[0][r], s_m[1][r]), fmaxf(s_m[2][r], s_m[3][r]));
-    if (mx == kNegInf) mx = 0.f;
-    float o = 0.f, den = 0.f;
-#pragma unroll
-    for (int w4 = 0; w4 < 4; ++w4) {
-      const float sc = exp2f(s_m[w4][r] - mx);
-      o += sc * s_o[w4][r * OS + c];
-      den += sc * s_l[w4][r];
+  auto start_batch = [&]() {
+    batch_len = min(kBatch, my_chunks - batch_base);
+    decode_batch(batch_base, batch_len);
+    ij = -1;
+    it = 0;
+    cj = 0;
+    for (int k = 0; k < NB; ++k) try_issue();
+  };
+
+  start_batch();
+  while (true) {
+    if (cj >= batch_len) {
+      batch_base += batch_len;
+      if (batch_base >= my_chunks) break;
+      wait_vmcnt<0>();  // ring and Q buffers idle before they are re-described
+      start_batch();
+      continue;
     }
-    p.ws_o[(prow0 + r) * DH + c] = o;
-    if (c == 0) {
-      p.ws_m[prow0 + r] = mx;
-      p.ws_l[prow0 + r] = den;
+    while (ij < cj) try_issue();  // enter this chunk (loads its Q)
+    const int b = desc[cj][0], kvh = desc[cj][1], rt = desc[cj][2], split = desc[cj][3];
+    const int pg0 = desc[cj][4], npg = desc[cj][5], S = desc[cj][6], nsb = desc[cj][7];
+    const int ntile = 2 * npg;
+    wait_tiles<NF>(n_issued - q_tiles_before[cj & 1]);
+    u32x4 qf[NQ][KS];
+    int cap_blk[NQ], cap_none[NQ];
+#pragma unroll
+    for (int qt = 0; qt < NQ; ++qt) {
+      cap_blk[qt] = (rt * ROWS + qt * 16 + ln) / p.group;  // block position i of the row
+      cap_none[qt] = 0x7fffffff;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+        qf[qt][ks] = *reinterpret_cast<const u32x4 *>(qbuf[cj & 1] + (qt * KS + ks) * kFragBytes + 16 * lane);
+    }
+    State<DH, NQ> st;
+#pragma unroll
+    for (int qt = 0; qt < NQ; ++qt) {
+      st.m[qt] = kNegInf;
+      st.l[qt] = 0.f;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) st.o[qt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    for (int t = 0; t < ntile; ++t) {
+      try_issue();
+      wait_tiles<NF>(n_issued - n_done - 1);
+      const uint8_t *slot = ring + (n_done % NB) * G::SLOT;
+      Frags<DH> f;
+#pragma unroll
+      for (int e = 0; e < 2; ++e)
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+          f.k[e][ks] = *reinterpret_cast<const u32x4 *>(slot + (e * KS + ks) * kFragBytes + 16 * lane);
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+        f.v[dt] = *reinterpret_cast<const u32x4 *>(slot + (2 * KS + dt) * kFragBytes + 16 * lane);
+      const int page = pid[cj][t >> 1];
+      const bool ok = page >= 0 && page < p.num_pages;
+      const int limit = ok ? min(32, S - (pg0 + (t >> 1)) * kPage - 32 * (t & 1)) : 0;
+      ++n_done;
+      compute_tile<DH, NQ>(st, f, qf, cap_none, limit, p.scale_log2, lg);
+    }
+    ++cj;
+    // keep the stream going into the next chunk while the block is computed
+    for (int k = 0; k < NB; ++k) try_issue();
+    if (split == 0) {
+      // the draft block: token-major rows of stride Hkv * DH, read directly;
+      // tokens past w are clamped to row w - 1 and masked
+      const bf16_t *kb = static_cast<const bf16_t *>(p.kb) +
+                         (static_cast<size_t>(b) * p.w * p.hkv + kvh) * DH;
+      const bf16_t *vb = static_cast<const bf16_t *>(p.vb) +
+                         (static_cast<size_t>(b) * p.w * p.hkv + kvh) * DH;
+      for (int u = 0; u * 32 < p.w; ++u) {
+        Frags<DH> f;
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+          const int tok = min(slot_token(2 * u + e, ln), p.w - 1);
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks) f.k[e][ks] = load16(kb + tok * tok_stride + 32 * ks + 8 * lg);
+        }
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+          u16x8 v8;
+#pragma unroll
+          for (int jj = 0; jj < 8; ++jj) {
+            const int tok = min(32 * u + 8 * lg + jj, p.w - 1);
+            v8[jj] = vb[tok * tok_stride + 16 * dt + ln];
+          }
+          f.v[dt] = __builtin_bit_cast(u32x4, v8);
+        }
+        int cap[NQ];
+#pragma unroll
+        for (int qt = 0; qt < NQ; ++qt) cap[qt] = cap_blk[qt] - 32 * u;
+        compute_tile<DH, NQ>(st, f, qf, cap, p.w - 32 * u, p.scale_log2, lg);
+      }
+    }
+
+    // Chunk result. Lane holds head dims 16dt + 4g .. +3 of row n of tile qt.
+    const size_t prow0 = ((static_cast<size_t>(b) * p.hkv + kvh) * p.nsplit + split) * p.rows;
+#pragma unroll
+    for (int qt = 0; qt < NQ; ++qt) {
+      const int row = rt * ROWS + qt * 16 + ln;
+      if (row >= p.rows) continue;
+      if (nsb == 1) {
+        const float inv = 1.f / st.l[qt];
+        const int i = row / p.group, h = kvh * p.group + row % p.group;
+        bf16_t *orow = static_cast<bf16_t *>(p.out) +
+                       ((static_cast<size_t>(b) * p.w + i) * p.hq + h) * DH;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+          const f32x4 o = st.o[qt][dt];
+          u32x2 packed;
+          packed[0] = static_cast<uint32_t>(f32_to_bf16(o[0] * inv)) |
+                      (static_cast<uint32_t>(f32_to_bf16(o[1] * inv)) << 16);
+          packed[1] = static_cast<uint32_t>(f32_to_bf16(o[2] * inv)) |
+                      (static_cast<uint32_t>(f32_to_bf16(o[3] * inv)) << 16);
+          *reinterpret_cast<u32x2 *>(orow + 16 * dt + 4 * lg) = packed;
+        }
+        if (lg == 0 && p.lse)
+          p.lse[(static_cast<size_t>(b) * p.hq + h) * p.w + i] =
+              (st.m[qt] + log2f(st.l[qt])) * 0.69314718055994530942f;
+      } else {
+        float *orow = p.ws_o + (prow0 + row) * DH;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) *reinterpret_cast<f32x4 *>(orow + 16 * dt + 4 * lg) = st.o[qt][dt];
+        if (lg == 0) {
+          p.ws_m[prow0 + row] = st.m[qt] == kNegInf ? 0.f : st.m[qt];
+          p.ws_l[prow0 + row] = st.l[qt];
+        }
+      }
     }
   }
 }
 
-template <int DH, int NQ>
-hipError_t launch_typed(const AttnParams &p, hipStream_t s) {
+// Workers resident per compute unit, from the LDS each one needs.
+template <int DH, int NQ, int NB>
+constexpr int workers_per_cu() {
+  constexpr int n = (160 * 1024) / Geo<DH, NQ, NB>::LDS;
+  return n > 8 ? 8 : (n < 1 ? 1 : n);
+}
+
+template <int DH, int NQ, int NB>
+hipError_t launch_typed(const AttnParams &p, int n_cu, hipStream_t s) {
   const int n_rt = (p.rows + 16 * NQ - 1) / (16 * NQ);
-  const int n_items = p.batch * p.hkv * p.nsplit;
-  const int grid = ((n_items + 7) / 8) * 8 * n_rt;
-  hipLaunchKernelGGL((attn_mfma_kernel<DH, NQ>), dim3(grid), dim3(256), 0, s, p, n_rt, n_items);
+  const int workers = n_cu * workers_per_cu<DH, NQ, NB>();
+  hipLaunchKernelGGL((attn_mfma_kernel<DH, NQ, NB>), dim3(workers), dim3(64), 0, s, p, n_rt,
+                     workers);
   return hipGetLastError();
+}
+
+template <int DH>
+hipError_t launch_dh(const AttnParams &p, int n_cu, hipStream_t s) {
+  constexpr int NB = DH == 128 ? 2 : 3;
+  if (p.rows <= 16) return launch_typed<DH, 1, NB>(p, n_cu, s);
+  if (p.rows <= 32) return launch_typed<DH, 2, NB>(p, n_cu, s);
+  return launch_typed<DH, 4, 2>(p, n_cu, s);
 }
 
 }  // namespace
 
-int mfma_rows_per_wg(int rows) { return rows <= 16 ? 16 : 32; }
+int mfma_rows_per_wg(int rows) { return rows <= 16 ? 16 : (rows <= 32 ? 32 : 64); }
 
 hipError_t launch_attn_mfma(const AttnParams &p, int dh, hipStream_t s) {
-  const bool one = p.rows <= 16;
-  if (dh == 64) return one ? launch_typed<64, 1>(p, s) : launch_typed<64, 2>(p, s);
-  if (dh == 96) return one ? launch_typed<96, 1>(p, s) : launch_typed<96, 2>(p, s);
-  return one ? launch_typed<128, 1>(p, s) : launch_typed<128, 2>(p, s);
+  int dev = 0, n_cu = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return hipErrorInvalidDevice;
+  if (hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return hipErrorInvalidDevice;
+  n_cu = (n_cu + 7) / 8 * 8;  // the worker ranking assumes a multiple of 8
+  if (dh == 64) return launch_dh<64>(p, n_cu, s);
+  if (dh == 96) return launch_dh<96>(p, n_cu, s);
+  return launch_dh<128>(p, n_cu, s);
 }
 
 }  // namespace das

@@ -10,7 +10,7 @@
 namespace das {
 
 constexpr int kPage = DAS_PAGE_TOKENS;  // tokens per cache page
-constexpr int kMaxPagesPerSplit = 128;  // matrix-core kernel: page ids held one per lane
+constexpr int kMaxPagesPerSplit = 64;   // matrix-core kernel: one page id per lane
 
 // Everything one attention launch needs. Pointers are device pointers; the
 // pool pointers already include the plane and core-layer offsets, so a
