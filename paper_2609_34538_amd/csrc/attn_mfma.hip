@@ -9,14 +9,16 @@
 // gets about the same number of full chunks, and consecutive chunks (the row
 // tiles of one split) land on the same XCD and share its L2.
 //
-// Each worker streams the half pages (32 tokens) of its chunks, one chunk
-// after the other, through a private ring of NB LDS slots filled by the
-// direct-to-LDS loads of gfx950 (global_load_lds_dwordx4), up to NB tiles
-// ahead of the tile being computed and across chunk boundaries; each chunk's
-// Q fragments are loaded into one of two LDS buffers the same way when the
-// stream enters the chunk. The worker waits on its own vector-memory counter
-// for the data it reads. Chunk descriptors and page ids are decoded into LDS
-// a batch of chunks at a time.
+// Each worker streams the 32-token tiles of its chunks (two per prefix page,
+// then the draft block's), one chunk after the other, through a private
+// ring of NB LDS slots filled by the direct-to-LDS loads of gfx950
+// (global_load_lds_dwordx4), up to NB tiles ahead of the tile being computed
+// and across chunk boundaries; a chunk's Q fragments go into one of two LDS
+// buffers the same way when the stream enters the chunk. The worker waits on
+// its own vector-memory counter for the data it reads. Load addresses are a
+// uniform base (page, fragment) plus one per-lane offset, so issuing a tile
+// costs no per-lane address arithmetic. Chunk descriptors and page ids are
+// decoded a batch of chunks at a time into registers.
 //
 // Both products run on v_mfma_f32_16x16x32_bf16 with the key/value tile as
 // the A operand, so softmax probabilities never leave registers:
@@ -25,11 +27,12 @@
 // MFMA 16x16x32 bf16 lane layout (lane l, n = l % 16, g = l / 16):
 //   A[m][k]: lane holds m = n, k = 8g..8g+7   B[k][n]: k = 8g..8g+7, n
 //   C[m][n]: lane holds m = 4g..4g+3, n
-// The 16 token slots of each S^T tile are a permutation of the page tokens
-// chosen so that the C fragments of tiles 2u and 2u+1 hold, per lane, the 8
-// consecutive tokens 32u + 8g .. 32u + 8g + 7; those are exactly the k slots
-// of the P^T fragment of the P.V product, and the matching V^T fragment is
-// one contiguous 16-byte load from the dim-major value page.
+// The 16 token slots of each S^T tile are a permutation of the tile's tokens
+// chosen so that the C fragments of the tile's two S^T halves hold, per lane,
+// the 8 consecutive tokens 8g .. 8g + 7; those are exactly the k slots of the
+// P^T fragment of the P.V product, and the matching V^T fragment is one
+// contiguous 16-byte load from the dim-major value page. The draft block's
+// values are token-major; their V^T fragments are gathered from LDS.
 //
 // A chunk ends by writing its (m, l, O) partial to the workspace for the
 // combine kernel, or, when its sequence has a single split, the normalised
@@ -49,15 +52,11 @@ typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
 
 constexpr float kNegInf = -__builtin_huge_valf();
 constexpr int kFragBytes = 64 * 16;  // one 16-byte fragment per lane
-constexpr int kBatch = 8;            // chunk descriptors decoded at a time
+constexpr int kBatch = 8;            // chunks decoded at a time (8 fields each)
 constexpr int kMaxSeqBlocks = 64;    // sequences are scanned 64 at a time
 
-__device__ __forceinline__ u32x4 load16(const bf16_t *ptr) {
-  return *reinterpret_cast<const u32x4 *>(ptr);
-}
-
 // 16 bytes per lane, global -> LDS at lds + 16 * lane (lds wave-uniform).
-__device__ __forceinline__ void dma16(const bf16_t *src, uint8_t *lds) {
+__device__ __forceinline__ void dma16(const void *src, uint8_t *lds) {
   __builtin_amdgcn_global_load_lds((__attribute__((address_space(1))) void *)(src),
                                    (__attribute__((address_space(3))) void *)(lds), 16, 0, 0);
 }
@@ -69,8 +68,8 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
-// Wait until at most `tiles` page tiles of NF loads each are outstanding.
-// Any other loads issued later only make the wait stricter.
+// Wait until at most `tiles` tiles of NF loads each are outstanding. Other
+// loads or stores issued later only make the wait stricter.
 template <int NF>
 __device__ __forceinline__ void wait_tiles(int tiles) {
   if (tiles <= 0) wait_vmcnt<0>();
@@ -84,20 +83,17 @@ __device__ __forceinline__ f32x4 mfma16x16x32(u32x4 a, u32x4 b, f32x4 c) {
                                                  __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 
-// Token of the page/block held in slot m of S^T tile tt (see header comment).
-__device__ __forceinline__ int slot_token(int tt, int m) {
-  return 32 * (tt >> 1) + 8 * (m >> 2) + 4 * (tt & 1) + (m & 3);
-}
+__device__ __forceinline__ int uni(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
 template <int DH, int NQ, int NB_>
 struct Geo {
   static constexpr int KS = DH / 32;       // k steps of Q K^T
   static constexpr int DT = DH / 16;       // head-dim tiles of P V
-  static constexpr int NF = 2 * KS + DT;   // fragments (loads) per half-page tile
+  static constexpr int NF = 2 * KS + DT;   // fragments (loads) per 32-token tile
   static constexpr int SLOT = NF * kFragBytes;
   static constexpr int NB = NB_;           // ring depth
   static constexpr int QF = NQ * KS;       // Q fragments of a row tile
-  static constexpr int LDS = NB * SLOT + 2 * QF * kFragBytes + kBatch * (8 + 64) * 4 +
+  static constexpr int LDS = NB * SLOT + 2 * QF * kFragBytes + kBatch * 64 * 4 +
                              2 * kMaxSeqBlocks * 4;
 };
 
@@ -107,23 +103,18 @@ struct State {
   f32x4 o[NQ][DH / 16];
 };
 
-// Key (2 x KS) and value (DT) fragments of one 32-token tile.
-template <int DH>
-struct Frags {
-  u32x4 k[2][DH / 32];
-  u32x4 v[DH / 16];
-};
-
 // One 32-token tile through both products and the online softmax. Token t of
-// the tile (0..31) is visible when t < limit and t <= cap (cap = i - 32u for
-// the draft block's half u, unbounded for prefix pages).
+// the tile (0..31) is visible when t < limit and t <= cap[qt]; a full tile
+// (every token visible) skips the mask.
 template <int DH, int NQ>
-__device__ __forceinline__ void compute_tile(State<DH, NQ> &st, const Frags<DH> &f,
+__device__ __forceinline__ void compute_tile(State<DH, NQ> &st, const u32x4 (&kf)[2][DH / 32],
+                                             const u32x4 (&vf)[DH / 16],
                                              const u32x4 (&qf)[NQ][DH / 32],
-                                             const int (&cap)[NQ], int limit, float scale,
-                                             int lg) {
+                                             const int (&cap)[NQ], int limit, bool full,
+                                             float scale, int lg) {
   u16x8 pf[NQ];
   float alpha[NQ];
+  bool moved = false;
 #pragma unroll
   for (int qt = 0; qt < NQ; ++qt) {
     f32x4 sacc[2];
@@ -131,7 +122,7 @@ __device__ __forceinline__ void compute_tile(State<DH, NQ> &st, const Frags<DH> 
     for (int e = 0; e < 2; ++e) {
       sacc[e] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int ks = 0; ks < DH / 32; ++ks) sacc[e] = mfma16x16x32(f.k[e][ks], qf[qt][ks], sacc[e]);
+      for (int ks = 0; ks < DH / 32; ++ks) sacc[e] = mfma16x16x32(kf[e][ks], qf[qt][ks], sacc[e]);
     }
     float x[2][4];
     float mx = kNegInf;
@@ -140,7 +131,7 @@ __device__ __forceinline__ void compute_tile(State<DH, NQ> &st, const Frags<DH> 
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
         const int t = 8 * lg + 4 * e + v;
-        const bool vis = (t < limit) & (t <= cap[qt]);
+        const bool vis = full || ((t < limit) & (t <= cap[qt]));
         x[e][v] = vis ? sacc[e][v] * scale : kNegInf;
         mx = fmaxf(mx, x[e][v]);
       }
@@ -149,15 +140,16 @@ __device__ __forceinline__ void compute_tile(State<DH, NQ> &st, const Frags<DH> 
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
     const float mnew = fmaxf(st.m[qt], mx);
     const float muse = mnew == kNegInf ? 0.f : mnew;
-    alpha[qt] = exp2f(st.m[qt] - muse);
+    alpha[qt] = __builtin_amdgcn_exp2f(st.m[qt] - muse);
+    moved |= alpha[qt] != 1.f;
     float psum = 0.f;
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
-        const __bf16 pb = static_cast<__bf16>(exp2f(x[e][v] - muse));
-        psum += static_cast<float>(pb);
-        pf[qt][4 * e + v] = __builtin_bit_cast(uint16_t, pb);
+        const float pv = __builtin_amdgcn_exp2f(x[e][v] - muse);
+        psum += pv;
+        pf[qt][4 * e + v] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(pv));
       }
     }
     psum += __shfl_xor(psum, 16, 64);
@@ -165,11 +157,18 @@ __device__ __forceinline__ void compute_tile(State<DH, NQ> &st, const Frags<DH> 
     st.l[qt] = st.l[qt] * alpha[qt] + psum;
     st.m[qt] = mnew;
   }
+  // rescale the accumulators only when some row's maximum moved
+  if (__builtin_amdgcn_ballot_w64(moved) != 0) {
+#pragma unroll
+    for (int qt = 0; qt < NQ; ++qt)
+#pragma unroll
+      for (int dt = 0; dt < DH / 16; ++dt) st.o[qt][dt] *= alpha[qt];
+  }
 #pragma unroll
   for (int dt = 0; dt < DH / 16; ++dt) {
 #pragma unroll
     for (int qt = 0; qt < NQ; ++qt)
-      st.o[qt][dt] = mfma16x16x32(f.v[dt], __builtin_bit_cast(u32x4, pf[qt]), st.o[qt][dt] * alpha[qt]);
+      st.o[qt][dt] = mfma16x16x32(vf[dt], __builtin_bit_cast(u32x4, pf[qt]), st.o[qt][dt]);
   }
 }
 
@@ -183,6 +182,9 @@ struct SeqBlock {
   int inclF, inclP; // inclusive prefix sums over the block's lanes
 };
 
+// Fields of a decoded chunk, lane 8j + f of the descriptor register.
+enum { F_B = 0, F_KVH, F_RT, F_SPLIT, F_PG0, F_NPG, F_S, F_NSB };
+
 template <int DH, int NQ, int NB>
 __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, int n_workers) {
   using G = Geo<DH, NQ, NB>;
@@ -192,8 +194,7 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, i
   constexpr int ROWS = 16 * NQ;
   __shared__ __attribute__((aligned(16))) uint8_t ring[NB * G::SLOT];
   __shared__ __attribute__((aligned(16))) uint8_t qbuf[2][G::QF * kFragBytes];
-  __shared__ int desc[kBatch][8];      // b, kvh, rt, split, pg0, npg, S, nsplit_b
-  __shared__ int pid[kBatch][64];      // page ids of each chunk
+  __shared__ int pid[kBatch][64];      // page ids of each decoded chunk
   __shared__ int blkF[kMaxSeqBlocks];  // full-split chunks of each sequence block
   __shared__ int blkP[kMaxSeqBlocks];  // last-split chunks of each sequence block
 
@@ -205,6 +206,7 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, i
   const int pps = p.pages_per_split;
   const int units = p.hkv * n_rt;  // chunks per split of one sequence
   const int nblocks = (p.batch + 63) >> 6;
+  const int nblk = (p.w + 31) >> 5;  // draft-block tiles of a split-0 chunk
 
   SeqBlock sb;
   sb.k = -1;
@@ -248,7 +250,9 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, i
   const int my_chunks = rank < total ? (total - rank + n_workers - 1) / n_workers : 0;
   if (my_chunks == 0) return;
 
-  // Decode a batch of chunks into desc[] and pid[].
+  // Batch of decoded chunks: descv lane 8j + f = field f of chunk j, and
+  // pid[j][i] = page id of the chunk's i-th page.
+  int descv = 0;
   auto decode_batch = [&](int first, int count) {
     int pages[kBatch];
 #pragma unroll
@@ -275,43 +279,49 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, i
       const int S = __shfl(sb.S, lb, 64);
       const int npages = __shfl(sb.npages, lb, 64);
       const int full = npages / pps;
-      const int nsb = max(1, (npages + pps - 1) / pps);
       const int split = phase2 ? full : local / units;
       const int u = local % units;
       const int pg0 = split * pps;
       const int npg = max(0, min(pps, npages - pg0));
-      if (lane == 0) {
-        desc[j][0] = b;
-        desc[j][1] = u / n_rt;
-        desc[j][2] = u % n_rt;
-        desc[j][3] = split;
-        desc[j][4] = pg0;
-        desc[j][5] = npg;
-        desc[j][6] = S;
-        desc[j][7] = nsb;
-      }
+      const int nsb = max(1, (npages + pps - 1) / pps);
+      const int d = lane - 8 * j;
+      descv = d == F_B ? b : descv;
+      descv = d == F_KVH ? u / n_rt : descv;
+      descv = d == F_RT ? u % n_rt : descv;
+      descv = d == F_SPLIT ? split : descv;
+      descv = d == F_PG0 ? pg0 : descv;
+      descv = d == F_NPG ? npg : descv;
+      descv = d == F_S ? S : descv;
+      descv = d == F_NSB ? nsb : descv;
       if (lane < npg) pages[j] = p.block_table[static_cast<size_t>(b) * p.max_pages + pg0 + lane];
     }
 #pragma unroll
-    for (int j = 0; j < kBatch; ++j)
-      if (j < count) pid[j][lane] = pages[j];
+    for (int j = 0; j < kBatch; ++j) pid[j][lane] = pages[j];
   };
+  auto field = [&](int j, int f) { return __builtin_amdgcn_readlane(descv, 8 * j + f); };
+  auto pages_of = [&](int j) { return pid[j][lane]; };
 
-  const bf16_t *kl = static_cast<const bf16_t *>(p.k_layer);
-  const bf16_t *vl = static_cast<const bf16_t *>(p.v_layer);
-  const size_t head_elems = static_cast<size_t>(p.num_pages) * kPage * DH;
-  const size_t tok_stride = static_cast<size_t>(p.hkv) * DH;
+  const char *kl = static_cast<const char *>(p.k_layer);
+  const char *vl = static_cast<const char *>(p.v_layer);
+  const size_t head_bytes = static_cast<size_t>(p.num_pages) * kPage * DH * 2;
+  const size_t tok_bytes = static_cast<size_t>(p.hkv) * DH * 2;  // block row stride
+  // per-lane byte offsets of the fragments inside a page: key token slot
+  // 8(n/4) + n%4 (plus a uniform part), column 8g; value row n, token 8g
+  const uint32_t lane_k = ((8 * (ln >> 2) + (ln & 3)) * DH + 8 * lg) * 2;
+  const uint32_t lane_v = (ln * kPage + 8 * lg) * 2;
 
-  // Issue cursor: chunk ij of the batch (entered: its Q is loading), next
-  // half-page tile it; n_issued page tiles so far. Compute cursor: chunk cj,
-  // n_done page tiles consumed. Q of batch chunk j sits in qbuf[j & 1].
+  // Issue cursor: batch chunk ij, next tile it of its ntile (= 2 npg page
+  // tiles, then nblk block tiles on split 0); n_issued tiles so far. Compute
+  // cursor: chunk cj, n_done tiles consumed. Q of batch chunk j sits in
+  // qbuf[j & 1].
   int batch_base = 0, batch_len = 0;
-  int ij = -1, it = 0, n_issued = 0;
+  int ij = -1, it = 0, i_ntile = 0, i_npg2 = 0, i_kvh = 0, i_b = 0;
+  int i_pages = 0;
+  int n_issued = 0;
   int cj = 0, n_done = 0;
-  int q_tiles_before[2] = {0, 0};  // n_issued when each Q buffer was loaded
+  int q_tiles0 = 0, q_tiles1 = 0;  // n_issued when each Q buffer was loaded
 
-  auto issue_q = [&](int j) {
-    const int b = desc[j][0], kvh = desc[j][1], rt = desc[j][2];
+  auto issue_q = [&](int j, int b, int kvh, int rt) {
     uint8_t *qb = qbuf[j & 1];
 #pragma unroll
     for (int qt = 0; qt < NQ; ++qt) {
@@ -323,33 +333,55 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, i
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) dma16(qrow + 32 * ks + 8 * lg, qb + (qt * KS + ks) * kFragBytes);
     }
-    q_tiles_before[j & 1] = n_issued;
+    if (j & 1) q_tiles1 = n_issued;
+    else q_tiles0 = n_issued;
   };
 
-  // Put one more page tile in the ring if there is room, entering the next
-  // chunk when the current one is exhausted (at most one chunk ahead of the
-  // compute cursor, so both Q buffers stay valid).
+  // Put one more tile in the ring if there is room, entering the next chunk
+  // when the current one is exhausted (at most one chunk ahead of the compute
+  // cursor, so both Q buffers stay valid).
   auto try_issue = [&]() {
     while (true) {
-      if (ij >= 0 && it < 2 * desc[ij][5]) {
+      if (ij >= 0 && it < i_ntile) {
         if (n_issued - n_done >= NB) return;
-        const int kvh = desc[ij][1];
-        const int page = pid[ij][it >> 1];
-        const bool ok = page >= 0 && page < p.num_pages;
-        if (!ok) report_error(p.dev_error, DAS_DEVERR_PAGE);
-        const size_t off = kvh * head_elems + static_cast<size_t>(ok ? page : 0) * kPage * DH;
         uint8_t *slot = ring + (n_issued % NB) * G::SLOT;
-        const int u = it & 1;
+        if (it < i_npg2) {
+          const int page = __builtin_amdgcn_readlane(i_pages, it >> 1);
+          const bool ok = page >= 0 && page < p.num_pages;
+          if (!ok) report_error(p.dev_error, DAS_DEVERR_PAGE);
+          const size_t off = i_kvh * head_bytes + static_cast<size_t>(ok ? page : 0) * kPage * DH * 2;
+          const int u = it & 1;
+          const char *kb = kl + off + (32 * u) * DH * 2;
+          const char *vb = vl + off + (32 * u) * 2;
 #pragma unroll
-        for (int e = 0; e < 2; ++e) {
-          const int tok = slot_token(2 * u + e, ln);
+          for (int e = 0; e < 2; ++e)
 #pragma unroll
-          for (int ks = 0; ks < KS; ++ks)
-            dma16(kl + off + tok * DH + 32 * ks + 8 * lg, slot + (e * KS + ks) * kFragBytes);
+            for (int ks = 0; ks < KS; ++ks)
+              dma16(kb + (4 * e * DH + 32 * ks) * 2 + lane_k, slot + (e * KS + ks) * kFragBytes);
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt)
+            dma16(vb + (16 * dt * kPage) * 2 + lane_v, slot + (2 * KS + dt) * kFragBytes);
+        } else {
+          // draft block tile u: key fragments by token slot, value rows raw
+          const int u = it - i_npg2;
+          const char *kb = static_cast<const char *>(p.kb) +
+                           (static_cast<size_t>(i_b) * p.w * p.hkv + i_kvh) * DH * 2;
+          const char *vb = static_cast<const char *>(p.vb) +
+                           (static_cast<size_t>(i_b) * p.w * p.hkv + i_kvh) * DH * 2;
+#pragma unroll
+          for (int e = 0; e < 2; ++e) {
+            const int tok = min(32 * u + 8 * (ln >> 2) + 4 * e + (ln & 3), p.w - 1);
+#pragma unroll
+            for (int ks = 0; ks < KS; ++ks)
+              dma16(kb + tok * tok_bytes + (32 * ks + 8 * lg) * 2, slot + (e * KS + ks) * kFragBytes);
+          }
+#pragma unroll
+          for (int f = 0; f < DT; ++f) {
+            const int o = f * kFragBytes + 16 * lane;  // byte in the [32][DH] half
+            const int tok = min(32 * u + o / (2 * DH), p.w - 1);
+            dma16(vb + tok * tok_bytes + o % (2 * DH), slot + (2 * KS + f) * kFragBytes);
+          }
         }
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt)
-          dma16(vl + off + (16 * dt + ln) * kPage + 32 * u + 8 * lg, slot + (2 * KS + dt) * kFragBytes);
         ++n_issued;
         ++it;
         return;
@@ -358,7 +390,12 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, i
       if (nj >= batch_len || nj > cj + 1) return;
       ij = nj;
       it = 0;
-      issue_q(nj);
+      i_b = uni(field(nj, F_B));
+      i_kvh = uni(field(nj, F_KVH));
+      i_npg2 = 2 * uni(field(nj, F_NPG));
+      i_ntile = i_npg2 + (uni(field(nj, F_SPLIT)) == 0 ? nblk : 0);
+      i_pages = pages_of(nj);
+      issue_q(nj, i_b, i_kvh, uni(field(nj, F_RT)));
     }
   };
 
@@ -376,21 +413,22 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, i
     if (cj >= batch_len) {
       batch_base += batch_len;
       if (batch_base >= my_chunks) break;
-      wait_vmcnt<0>();  // ring and Q buffers idle before they are re-described
+      wait_vmcnt<0>();  // ring and Q buffers idle before the next batch
       start_batch();
       continue;
     }
     while (ij < cj) try_issue();  // enter this chunk (loads its Q)
-    const int b = desc[cj][0], kvh = desc[cj][1], rt = desc[cj][2], split = desc[cj][3];
-    const int pg0 = desc[cj][4], npg = desc[cj][5], S = desc[cj][6], nsb = desc[cj][7];
-    const int ntile = 2 * npg;
-    wait_tiles<NF>(n_issued - q_tiles_before[cj & 1]);
+    const int b = uni(field(cj, F_B)), kvh = uni(field(cj, F_KVH)), rt = uni(field(cj, F_RT));
+    const int split = uni(field(cj, F_SPLIT)), pg0 = uni(field(cj, F_PG0));
+    const int npg = uni(field(cj, F_NPG)), S = uni(field(cj, F_S)), nsb = uni(field(cj, F_NSB));
+    const int c_pages = pages_of(cj);
+    const int ntile = 2 * npg + (split == 0 ? nblk : 0);
+    wait_tiles<NF>(n_issued - ((cj & 1) ? q_tiles1 : q_tiles0));
     u32x4 qf[NQ][KS];
-    int cap_blk[NQ], cap_none[NQ];
+    int cap_blk[NQ];
 #pragma unroll
     for (int qt = 0; qt < NQ; ++qt) {
       cap_blk[qt] = (rt * ROWS + qt * 16 + ln) / p.group;  // block position i of the row
-      cap_none[qt] = 0x7fffffff;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks)
         qf[qt][ks] = *reinterpret_cast<const u32x4 *>(qbuf[cj & 1] + (qt * KS + ks) * kFragBytes + 16 * lane);
@@ -407,55 +445,46 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, i
       try_issue();
       wait_tiles<NF>(n_issued - n_done - 1);
       const uint8_t *slot = ring + (n_done % NB) * G::SLOT;
-      Frags<DH> f;
+      ++n_done;
+      u32x4 kf[2][KS], vf[DT];
 #pragma unroll
       for (int e = 0; e < 2; ++e)
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
-          f.k[e][ks] = *reinterpret_cast<const u32x4 *>(slot + (e * KS + ks) * kFragBytes + 16 * lane);
+          kf[e][ks] = *reinterpret_cast<const u32x4 *>(slot + (e * KS + ks) * kFragBytes + 16 * lane);
+      int cap[NQ];
+      int limit;
+      bool full;
+      if (t < 2 * npg) {
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
-        f.v[dt] = *reinterpret_cast<const u32x4 *>(slot + (2 * KS + dt) * kFragBytes + 16 * lane);
-      const int page = pid[cj][t >> 1];
-      const bool ok = page >= 0 && page < p.num_pages;
-      const int limit = ok ? min(32, S - (pg0 + (t >> 1)) * kPage - 32 * (t & 1)) : 0;
-      ++n_done;
-      compute_tile<DH, NQ>(st, f, qf, cap_none, limit, p.scale_log2, lg);
-    }
-    ++cj;
-    // keep the stream going into the next chunk while the block is computed
-    for (int k = 0; k < NB; ++k) try_issue();
-    if (split == 0) {
-      // the draft block: token-major rows of stride Hkv * DH, read directly;
-      // tokens past w are clamped to row w - 1 and masked
-      const bf16_t *kb = static_cast<const bf16_t *>(p.kb) +
-                         (static_cast<size_t>(b) * p.w * p.hkv + kvh) * DH;
-      const bf16_t *vb = static_cast<const bf16_t *>(p.vb) +
-                         (static_cast<size_t>(b) * p.w * p.hkv + kvh) * DH;
-      for (int u = 0; u * 32 < p.w; ++u) {
-        Frags<DH> f;
+        for (int dt = 0; dt < DT; ++dt)
+          vf[dt] = *reinterpret_cast<const u32x4 *>(slot + (2 * KS + dt) * kFragBytes + 16 * lane);
+        const int page = __builtin_amdgcn_readlane(c_pages, t >> 1);
+        const bool ok = page >= 0 && page < p.num_pages;
+        limit = ok ? min(32, S - (pg0 + (t >> 1)) * kPage - 32 * (t & 1)) : 0;
+        full = limit >= 32;
 #pragma unroll
-        for (int e = 0; e < 2; ++e) {
-          const int tok = min(slot_token(2 * u + e, ln), p.w - 1);
-#pragma unroll
-          for (int ks = 0; ks < KS; ++ks) f.k[e][ks] = load16(kb + tok * tok_stride + 32 * ks + 8 * lg);
-        }
+        for (int qt = 0; qt < NQ; ++qt) cap[qt] = 0x7fffffff;
+      } else {
+        // block values are token-major [32][DH] in the slot: gather V^T
+        const int u = t - 2 * npg;
+        const uint16_t *raw = reinterpret_cast<const uint16_t *>(slot + 2 * KS * kFragBytes);
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
           u16x8 v8;
 #pragma unroll
-          for (int jj = 0; jj < 8; ++jj) {
-            const int tok = min(32 * u + 8 * lg + jj, p.w - 1);
-            v8[jj] = vb[tok * tok_stride + 16 * dt + ln];
-          }
-          f.v[dt] = __builtin_bit_cast(u32x4, v8);
+          for (int jj = 0; jj < 8; ++jj) v8[jj] = raw[(8 * lg + jj) * DH + 16 * dt + ln];
+          vf[dt] = __builtin_bit_cast(u32x4, v8);
         }
-        int cap[NQ];
+        limit = p.w - 32 * u;
+        full = false;
 #pragma unroll
         for (int qt = 0; qt < NQ; ++qt) cap[qt] = cap_blk[qt] - 32 * u;
-        compute_tile<DH, NQ>(st, f, qf, cap, p.w - 32 * u, p.scale_log2, lg);
       }
+      compute_tile<DH, NQ>(st, kf, vf, qf, cap, limit, full, p.scale_log2, lg);
     }
+    ++cj;
+    for (int k = 0; k < NB; ++k) try_issue();  // keep the stream going into the next chunk
 
     // Chunk result. Lane holds head dims 16dt + 4g .. +3 of row n of tile qt.
     const size_t prow0 = ((static_cast<size_t>(b) * p.hkv + kvh) * p.nsplit + split) * p.rows;
@@ -512,15 +541,13 @@ hipError_t launch_typed(const AttnParams &p, int n_cu, hipStream_t s) {
 
 template <int DH>
 hipError_t launch_dh(const AttnParams &p, int n_cu, hipStream_t s) {
-  constexpr int NB = DH == 128 ? 2 : 3;
-  if (p.rows <= 16) return launch_typed<DH, 1, NB>(p, n_cu, s);
-  if (p.rows <= 32) return launch_typed<DH, 2, NB>(p, n_cu, s);
-  return launch_typed<DH, 4, 2>(p, n_cu, s);
+  if (p.rows <= 16) return launch_typed<DH, 1, 2>(p, n_cu, s);
+  return launch_typed<DH, 2, 2>(p, n_cu, s);
 }
 
 }  // namespace
 
-int mfma_rows_per_wg(int rows) { return rows <= 16 ? 16 : (rows <= 32 ? 32 : 64); }
+int mfma_rows_per_wg(int rows) { return rows <= 16 ? 16 : 32; }
 
 hipError_t launch_attn_mfma(const AttnParams &p, int dh, hipStream_t s) {
   int dev = 0, n_cu = 0;
