@@ -106,24 +106,32 @@ struct State {
 // One 32-token tile through both products and the online softmax. Token t of
 // the tile (0..31) is visible when t < limit and t <= cap[qt]; a full tile
 // (every token visible) skips the mask.
-template <int DH, int NQ>
+// `hook(k)` runs between the stages (k = 0 before the logits, 1 before the
+// softmax, 2 before P.V) so that the caller can spread work over the tile.
+template <int DH, int NQ, typename Hook>
 __device__ __forceinline__ void compute_tile(State<DH, NQ> &st, const u32x4 (&kf)[2][DH / 32],
                                              const u32x4 (&vf)[DH / 16],
                                              const u32x4 (&qf)[NQ][DH / 32],
                                              const int (&cap)[NQ], int limit, bool full,
-                                             float scale, int lg) {
+                                             float scale, int lg, Hook &&hook) {
   u16x8 pf[NQ];
   float alpha[NQ];
   bool moved = false;
+  f32x4 sacc[NQ][2];
+  hook(0);
 #pragma unroll
   for (int qt = 0; qt < NQ; ++qt) {
-    f32x4 sacc[2];
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
-      sacc[e] = f32x4{0.f, 0.f, 0.f, 0.f};
+      sacc[qt][e] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int ks = 0; ks < DH / 32; ++ks) sacc[e] = mfma16x16x32(kf[e][ks], qf[qt][ks], sacc[e]);
+      for (int ks = 0; ks < DH / 32; ++ks)
+        sacc[qt][e] = mfma16x16x32(kf[e][ks], qf[qt][ks], sacc[qt][e]);
     }
+  }
+  hook(1);
+#pragma unroll
+  for (int qt = 0; qt < NQ; ++qt) {
     float x[2][4];
     float mx = kNegInf;
 #pragma unroll
@@ -132,7 +140,7 @@ __device__ __forceinline__ void compute_tile(State<DH, NQ> &st, const u32x4 (&kf
       for (int v = 0; v < 4; ++v) {
         const int t = 8 * lg + 4 * e + v;
         const bool vis = full || ((t < limit) & (t <= cap[qt]));
-        x[e][v] = vis ? sacc[e][v] * scale : kNegInf;
+        x[e][v] = vis ? sacc[qt][e][v] * scale : kNegInf;
         mx = fmaxf(mx, x[e][v]);
       }
     }
@@ -157,6 +165,7 @@ __device__ __forceinline__ void compute_tile(State<DH, NQ> &st, const u32x4 (&kf
     st.l[qt] = st.l[qt] * alpha[qt] + psum;
     st.m[qt] = mnew;
   }
+  hook(2);
   // rescale the accumulators only when some row's maximum moved
   if (__builtin_amdgcn_ballot_w64(moved) != 0) {
 #pragma unroll
@@ -399,6 +408,82 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, i
     }
   };
 
+  // The same issue split in three parts (key fragments of each S^T half,
+  // then the values) so the loads of the next tile can be spread over the
+  // computation of the current one.
+  bool s_have = false;
+  bool s_blk = false;
+  const char *s_kb = nullptr, *s_vb = nullptr;
+  uint8_t *s_slot = nullptr;
+  int s_u = 0;
+  auto stage_begin = [&]() {
+    s_have = false;
+    while (true) {
+      if (ij >= 0 && it < i_ntile) {
+        if (n_issued - n_done >= NB) return;
+        s_have = true;
+        s_slot = ring + (n_issued % NB) * G::SLOT;
+        s_blk = it >= i_npg2;
+        if (!s_blk) {
+          const int page = __builtin_amdgcn_readlane(i_pages, it >> 1);
+          const bool ok = page >= 0 && page < p.num_pages;
+          if (!ok) report_error(p.dev_error, DAS_DEVERR_PAGE);
+          const size_t off = i_kvh * head_bytes + static_cast<size_t>(ok ? page : 0) * kPage * DH * 2;
+          s_u = it & 1;
+          s_kb = kl + off + (32 * s_u) * DH * 2;
+          s_vb = vl + off + (32 * s_u) * 2;
+        } else {
+          s_u = it - i_npg2;
+          s_kb = static_cast<const char *>(p.kb) + (static_cast<size_t>(i_b) * p.w * p.hkv + i_kvh) * DH * 2;
+          s_vb = static_cast<const char *>(p.vb) + (static_cast<size_t>(i_b) * p.w * p.hkv + i_kvh) * DH * 2;
+        }
+        return;
+      }
+      const int nj = ij + 1;
+      if (nj >= batch_len || nj > cj + 1) return;
+      ij = nj;
+      it = 0;
+      i_b = uni(field(nj, F_B));
+      i_kvh = uni(field(nj, F_KVH));
+      i_npg2 = 2 * uni(field(nj, F_NPG));
+      i_ntile = i_npg2 + (uni(field(nj, F_SPLIT)) == 0 ? nblk : 0);
+      i_pages = pages_of(nj);
+      issue_q(nj, i_b, i_kvh, uni(field(nj, F_RT)));
+    }
+  };
+  auto stage_part = [&](int part) {
+    if (!s_have) return;
+    if (part < 2) {
+      const int e = part;
+      if (!s_blk) {
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+          dma16(s_kb + (4 * e * DH + 32 * ks) * 2 + lane_k, s_slot + (e * KS + ks) * kFragBytes);
+      } else {
+        const int tok = min(32 * s_u + 8 * (ln >> 2) + 4 * e + (ln & 3), p.w - 1);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+          dma16(s_kb + tok * tok_bytes + (32 * ks + 8 * lg) * 2, s_slot + (e * KS + ks) * kFragBytes);
+      }
+    } else {
+      if (!s_blk) {
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+          dma16(s_vb + (16 * dt * kPage) * 2 + lane_v, s_slot + (2 * KS + dt) * kFragBytes);
+      } else {
+#pragma unroll
+        for (int f = 0; f < DT; ++f) {
+          const int o = f * kFragBytes + 16 * lane;  // byte in the [32][DH] half
+          const int tok = min(32 * s_u + o / (2 * DH), p.w - 1);
+          dma16(s_vb + tok * tok_bytes + o % (2 * DH), s_slot + (2 * KS + f) * kFragBytes);
+        }
+      }
+      ++n_issued;
+      ++it;
+      s_have = false;
+    }
+  };
+
   auto start_batch = [&]() {
     batch_len = min(kBatch, my_chunks - batch_base);
     decode_batch(batch_base, batch_len);
@@ -442,7 +527,6 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, i
       for (int dt = 0; dt < DT; ++dt) st.o[qt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
     for (int t = 0; t < ntile; ++t) {
-      try_issue();
       wait_tiles<NF>(n_issued - n_done - 1);
       const uint8_t *slot = ring + (n_done % NB) * G::SLOT;
       ++n_done;
@@ -481,7 +565,11 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, i
 #pragma unroll
         for (int qt = 0; qt < NQ; ++qt) cap[qt] = cap_blk[qt] - 32 * u;
       }
-      compute_tile<DH, NQ>(st, kf, vf, qf, cap, limit, full, p.scale_log2, lg);
+      // the slot's fragments are in registers before it is refilled
+      __builtin_amdgcn_s_waitcnt(0xF | (0x3 << 14) | (0x7 << 4));  // lgkmcnt(0)
+      stage_begin();
+      compute_tile<DH, NQ>(st, kf, vf, qf, cap, limit, full, p.scale_log2, lg,
+                           [&](int k) { stage_part(k); });
     }
     ++cj;
     for (int k = 0; k < NB; ++k) try_issue();  // keep the stream going into the next chunk
