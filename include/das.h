@@ -33,8 +33,9 @@
  *   kernels OR bits into it (DAS_DEVERR_*) for out-of-range page ids,
  *   prefix lengths or commit counts, and skip the offending data instead of
  *   reading or writing out of bounds.
- * - Reentrancy: the library holds no mutable global state; calls from
- *   several host threads are safe. Concurrent calls that share a workspace
+ * - Reentrancy: the only global state is a per-device cache of the compute
+ *   unit count, filled on first use; calls from several host threads are
+ *   safe. Concurrent calls that share a workspace
  *   or write the same cache rows race on the device, as any two kernels
  *   writing the same memory would.
  * - Numerics: scale is 1/sqrt(head_dim). Query head h reads KV head

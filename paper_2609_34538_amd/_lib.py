@@ -263,6 +263,51 @@ def attn_policy(cache: PagedCache, batch: Batch, layer: int, kappa: int, nu: int
     return out
 
 
+class PreparedAttention:
+    """One attention call with every argument marshalled up front, for loops
+    that issue the same call many times (the device buffers it names must
+    stay alive). Calling it enqueues the call on the stream captured here."""
+
+    def __init__(self, cache: PagedCache, batch: Batch, layer: int, kappa: int, nu: int,
+                 q: torch.Tensor, k_blk: torch.Tensor, v_blk: torch.Tensor,
+                 out: torch.Tensor, workspace: torch.Tensor, lse: Optional[torch.Tensor] = None,
+                 path: str = "auto", pages_per_split: int = 0, stream=None):
+        w, hq = _check_block(cache, batch, q, k_blk, v_blk)
+        if out.shape != q.shape or out.dtype != q.dtype or not out.is_contiguous():
+            raise ValueError("out must match q")
+        self._keep = (cache, batch, q, k_blk, v_blk, out, workspace, lse)
+        self._opts = _options(path, pages_per_split)
+        self._fn = LIB.das_attn_policy
+        self._args = (ctypes.byref(cache.c), ctypes.byref(batch.c), layer, kappa, nu, hq, w,
+                      q.data_ptr(), k_blk.data_ptr(), v_blk.data_ptr(), out.data_ptr(),
+                      _ptr(lse), workspace.data_ptr(), workspace.numel(),
+                      ctypes.byref(self._opts), _stream_handle(stream))
+
+    def __call__(self):
+        st = self._fn(*self._args)
+        if st != DAS_OK:
+            raise DasError(st, "das_attn_policy")
+
+
+class PreparedAppend:
+    """A commit call with its arguments marshalled up front."""
+
+    def __init__(self, cache: PagedCache, batch: Batch, k_new: torch.Tensor, v_new: torch.Tensor,
+                 num_new: torch.Tensor, len_out: Optional[torch.Tensor] = None, stream=None):
+        if k_new.dim() != 6 or num_new.dtype != torch.int32:
+            raise ValueError("k_new must be 6-d and num_new int32")
+        self._keep = (cache, batch, k_new, v_new, num_new, len_out)
+        self._fn = LIB.das_kv_append
+        self._args = (ctypes.byref(cache.c), ctypes.byref(batch.c), k_new.data_ptr(),
+                      v_new.data_ptr(), k_new.shape[3], num_new.data_ptr(), _ptr(len_out),
+                      _stream_handle(stream))
+
+    def __call__(self):
+        st = self._fn(*self._args)
+        if st != DAS_OK:
+            raise DasError(st, "das_kv_append")
+
+
 def attn_draft_maturev(cache: PagedCache, batch: Batch, layer: int, draft_depth: int,
                        q, k_blk, v_blk, out=None, lse=None, workspace=None, stream=None):
     """Mature-V draft read: keys at draft_depth, values at the full depth R."""

@@ -39,10 +39,14 @@
 // output. Query rows of a row tile: row = i * G + g (block position i,
 // head kvh * G + g). Logits are scaled into base-2 units after the product.
 
+#include <atomic>
+
 #include "das_internal.h"
 
 namespace das {
 namespace {
+
+constexpr int kMaxDevices = 64;
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -637,12 +641,20 @@ hipError_t launch_dh(const AttnParams &p, int n_cu, hipStream_t s) {
 
 int mfma_rows_per_wg(int rows) { return rows <= 16 ? 16 : 32; }
 
+// Compute units of each device, queried once (0 = not yet known).
+std::atomic<int> g_cu_count[kMaxDevices];
+
 hipError_t launch_attn_mfma(const AttnParams &p, int dh, hipStream_t s) {
-  int dev = 0, n_cu = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return hipErrorInvalidDevice;
-  if (hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-    return hipErrorInvalidDevice;
-  n_cu = (n_cu + 7) / 8 * 8;  // the worker ranking assumes a multiple of 8
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return hipErrorInvalidDevice;
+  int n_cu = dev < kMaxDevices ? g_cu_count[dev].load(std::memory_order_relaxed) : 0;
+  if (n_cu == 0) {
+    if (hipDeviceGetAttribute(&n_cu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        n_cu < 1)
+      return hipErrorInvalidDevice;
+    n_cu = (n_cu + 7) / 8 * 8;  // the worker ranking assumes a multiple of 8
+    if (dev < kMaxDevices) g_cu_count[dev].store(n_cu, std::memory_order_relaxed);
+  }
   if (dh == 64) return launch_dh<64>(p, n_cu, s);
   if (dh == 96) return launch_dh<96>(p, n_cu, s);
   return launch_dh<128>(p, n_cu, s);
