@@ -50,6 +50,8 @@ def parse():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--attn-only", action="store_true",
                     help="profiling aid: time only the attention launches")
+    ap.add_argument("--eager", action="store_true",
+                    help="launch every call from the host instead of replaying HIP graphs")
     return ap.parse_args()
 
 
@@ -139,7 +141,12 @@ def main():
     outs = [torch.empty_like(q) for q, _, _ in draft_in]
     out_v = torch.empty_like(qv)
     len_out = torch.empty(wl.batch, dtype=torch.int32, device=dev)
-    stream = torch.cuda.current_stream()
+    # A stream of its own (default priority): graphs cannot be captured on
+    # the legacy default stream.
+    # Graph replays launch on the current stream, so it is made current.
+    stream = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    torch.cuda.set_stream(stream)
 
     # Every call of a step, marshalled once per cache copy: the Mature-V
     # draft of each layer (and round), the verifier of each layer, the commit.
@@ -150,31 +157,71 @@ def main():
             for r, (d, w) in enumerate(rounds):
                 q, kb, vb = draft_in[r]
                 seq.append((w, das.PreparedAttention(cache, batch, layer, d, R, q, kb, vb, outs[r],
-                                                     ws, **opts)))
+                                                     ws, stream=stream, **opts)))
         for layer in range(wl.layers):
             seq.append((wl.verify_width,
                         das.PreparedAttention(cache, batch, layer, R, R, qv, k_new[kp, layer],
-                                              v_new[vp, layer], out_v, ws, **opts)))
+                                              v_new[vp, layer], out_v, ws, stream=stream,
+                                              **opts)))
         if not args.attn_only:
-            seq.append((None, das.PreparedAppend(cache, batch, k_new, v_new, num_new_t, len_out)))
+            seq.append((None, das.PreparedAppend(cache, batch, k_new, v_new, num_new_t, len_out,
+                                                 stream=stream)))
         step_calls.append(seq)
     n_attn = sum(1 for w, _ in step_calls[0] if w is not None)
+    widths = [w for w, _ in step_calls[0] if w is not None]
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(n_attn * args.steps)]
-    ev_w = []
+          for _ in range(args.steps if not args.eager else n_attn * args.steps)]
+    spans = []  # (start event, end event, attention launches covered)
 
-    def step(i, timed):
-        k = 0
-        for w, call in step_calls[i % copies]:
-            if timed and w is not None:
-                e0, e1 = ev[(i * n_attn) + k]
+    if args.eager:
+        def step(i, timed):
+            k = 0
+            for w, call in step_calls[i % copies]:
+                if timed and w is not None:
+                    e0, e1 = ev[(i * n_attn) + k]
+                    e0.record(stream)
+                    call()
+                    e1.record(stream)
+                    spans.append((e0, e1, [w]))
+                    k += 1
+                else:
+                    call()
+    else:
+        # One graph per cache copy for the attention launches of a step and
+        # one for its commit; the timing events sit between the two replays.
+        for seq in step_calls:  # eager pass first: per-device state is set up
+            for _, call in seq:
+                call()
+        torch.cuda.synchronize()
+        graphs = []
+        for seq in step_calls:
+            g_attn = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g_attn, stream=stream):
+                for w, call in seq:
+                    if w is not None:
+                        call()
+            g_commit = None
+            if not args.attn_only:
+                g_commit = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g_commit, stream=stream):
+                    for w, call in seq:
+                        if w is None:
+                            call()
+            graphs.append((g_attn, g_commit))
+        torch.cuda.synchronize()
+
+        def step(i, timed):
+            g_attn, g_commit = graphs[i % copies]
+            if timed:
+                e0, e1 = ev[i]
                 e0.record(stream)
-                call()
+                g_attn.replay()
                 e1.record(stream)
-                ev_w.append((e0, e1, w))
-                k += 1
+                spans.append((e0, e1, widths))
             else:
-                call()
+                g_attn.replay()
+            if g_commit is not None:
+                g_commit.replay()
 
     for i in range(args.warmup):
         step(i, False)
@@ -192,9 +239,10 @@ def main():
     value = tokens_per_step / (ms_step / 1e3)
 
     # dominant kernel: the attention launches
-    durs = [(a.elapsed_time(b), w) for a, b, w in ev_w]
-    attn_ms = float(np.mean([d for d, _ in durs]))
-    bytes_per = float(np.mean([algorithmic_attn_bytes(wl, lens, w) for _, w in durs]))
+    attn_total_ms = sum(a.elapsed_time(b) for a, b, _ in spans)
+    launches = [w for _, _, ws_ in spans for w in ws_]
+    attn_ms = attn_total_ms / len(launches)
+    bytes_per = float(np.mean([algorithmic_attn_bytes(wl, lens, w) for w in launches]))
     achieved = bytes_per / (attn_ms / 1e3) / 1e9
     step_bytes = (sum(algorithmic_attn_bytes(wl, lens, w) for _, w in rounds) * wl.layers
                   + algorithmic_attn_bytes(wl, lens, wl.verify_width) * wl.layers
@@ -222,6 +270,7 @@ def main():
                    "verify": {"depth": R, "width": wl.verify_width}, "depth_R": R,
                    "core_layers": wl.layers, "path": args.path,
                    "pages_per_split": args.pps, "cache_copies_rotated": copies,
+                   "launch": "eager" if args.eager else "hip_graph",
                    "commit": not args.attn_only},
         "step_hbm_gbs": step_bytes / (ms_step / 1e3) / 1e9,
         "step_frac_of_8tbs": step_bytes / (ms_step / 1e3) / 1e9 / HBM_PEAK_GBS,

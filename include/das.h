@@ -38,6 +38,10 @@
  *   safe. Concurrent calls that share a workspace
  *   or write the same cache rows race on the device, as any two kernels
  *   writing the same memory would.
+ * - Alignment: the kernels move K/V/Q/O rows with 16-byte accesses, so
+ *   k_pool, v_pool, q, k_blk, v_blk, out, k_new and v_new must be 16-byte
+ *   aligned (any allocation, or a view starting on a row, is); int32 and
+ *   fp32 arrays must be 4-byte aligned. Otherwise DAS_ERR_ALIGN.
  * - Numerics: scale is 1/sqrt(head_dim). Query head h reads KV head
  *   h / (Hq / Hkv). Accumulation is fp32; outputs are rounded to the input
  *   dtype (round to nearest even).
@@ -68,7 +72,8 @@ typedef enum das_status {
   DAS_ERR_DTYPE = -4,       /* unknown element type                           */
   DAS_ERR_WORKSPACE = -5,   /* workspace missing or smaller than required     */
   DAS_ERR_HIP = -6,         /* a HIP launch failed                            */
-  DAS_ERR_UNSUPPORTED = -7  /* valid request that this build does not handle  */
+  DAS_ERR_UNSUPPORTED = -7, /* valid request that this build does not handle  */
+  DAS_ERR_ALIGN = -8        /* a device array is not aligned as required      */
 } das_status;
 
 typedef enum das_dtype { DAS_F32 = 0, DAS_BF16 = 1 } das_dtype;

@@ -4,10 +4,13 @@
 // (sequence, KV head, row tile of 16 * NQ query rows, prefix split of up to
 // pages_per_split pages); split 0 of every (sequence, head, row tile) also
 // carries the draft block. Chunks are enumerated with every full split first
-// and the shorter last splits after them, and worker r (ranked XCD-major)
-// takes chunks r, r + W, r + 2W, ... (W = number of workers): every worker
-// gets about the same number of full chunks, and consecutive chunks (the row
-// tiles of one split) land on the same XCD and share its L2.
+// and the shorter last splits after them, and worker r takes chunks r, r + W,
+// r + 2W, ... (W = number of workers, a multiple of 8): every worker gets
+// about the same number of full chunks. Workgroups are dealt to the 8 XCDs
+// round-robin, so chunk c runs on XCD c mod 8 and even a call with fewer
+// chunks than workers spreads over every XCD. Inside each run of 8 splits
+// the row tiles of one split are numbered 8 apart, which puts them on one
+// XCD, where they share its L2.
 //
 // Each worker streams the 32-token tiles of its chunks (two per prefix page,
 // then the draft block's), one chunk after the other, through a private
@@ -214,8 +217,7 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, i
   const int lane = threadIdx.x;
   const int ln = lane & 15;
   const int lg = lane >> 4;
-  // worker rank, XCD-major: workgroups are dealt to the 8 XCDs round-robin
-  const int rank = (blockIdx.x & 7) * (n_workers >> 3) + (blockIdx.x >> 3);
+  const int rank = blockIdx.x;  // runs on XCD rank mod 8
   const int pps = p.pages_per_split;
   const int units = p.hkv * n_rt;  // chunks per split of one sequence
   const int nblocks = (p.batch + 63) >> 6;
@@ -264,17 +266,29 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, i
   if (my_chunks == 0) return;
 
   // Batch of decoded chunks: descv lane 8j + f = field f of chunk j, and
-  // pid[j][i] = page id of the chunk's i-th page.
+  // pid[j][i] = page id of the chunk's i-th page. The descriptors are
+  // computed first and the page-table loads of the whole batch issued after
+  // them, so the batch costs one memory round trip.
   int descv = 0;
+  auto field = [&](int j, int f) { return __builtin_amdgcn_readlane(descv, 8 * j + f); };
   auto decode_batch = [&](int first, int count) {
-    int pages[kBatch];
 #pragma unroll
     for (int j = 0; j < kBatch; ++j) {
-      pages[j] = 0;
       if (j >= count) continue;
       const int c = rank + (first + j) * n_workers;
       const bool phase2 = c >= totF;
       int rem = phase2 ? c - totF : c;
+      // chunk number -> (split group, row tile): in each complete run of 8
+      // groups of n_rt row tiles, row tile rt of group 8k + x is number
+      // 8 n_rt k + 8 rt + x
+      {
+        const int span = 8 * n_rt;
+        const int runs = ((phase2 ? totP : totF) / n_rt) >> 3;
+        if (rem < runs * span) {
+          const int k = rem / span, x = rem % span;
+          rem = (8 * k + (x & 7)) * n_rt + (x >> 3);
+        }
+      }
       int k = 0;
       while (k < nblocks - 1) {
         const int n = phase2 ? blkP[k] : blkF[k];
@@ -306,12 +320,18 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, i
       descv = d == F_NPG ? npg : descv;
       descv = d == F_S ? S : descv;
       descv = d == F_NSB ? nsb : descv;
+    }
+    int pages[kBatch];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      pages[j] = 0;
+      const int b = uni(field(j, F_B)), pg0 = uni(field(j, F_PG0));
+      const int npg = j < count ? uni(field(j, F_NPG)) : 0;
       if (lane < npg) pages[j] = p.block_table[static_cast<size_t>(b) * p.max_pages + pg0 + lane];
     }
 #pragma unroll
     for (int j = 0; j < kBatch; ++j) pid[j][lane] = pages[j];
   };
-  auto field = [&](int j, int f) { return __builtin_amdgcn_readlane(descv, 8 * j + f); };
   auto pages_of = [&](int j) { return pid[j][lane]; };
 
   const char *kl = static_cast<const char *>(p.k_layer);

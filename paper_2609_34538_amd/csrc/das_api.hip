@@ -18,9 +18,12 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 int elem_bytes(int dtype) { return dtype == DAS_F32 ? 4 : 2; }
 
+bool aligned(const void *ptr, size_t a) { return reinterpret_cast<uintptr_t>(ptr) % a == 0; }
+
 das_status check_cache(const das_cache *c) {
   if (!c) return DAS_ERR_NULL;
   if (!c->k_pool || !c->v_pool) return DAS_ERR_NULL;
+  if (!aligned(c->k_pool, 16) || !aligned(c->v_pool, 16)) return DAS_ERR_ALIGN;
   if (c->dtype != DAS_F32 && c->dtype != DAS_BF16) return DAS_ERR_DTYPE;
   if (c->num_depths < 1 || c->num_depths > DAS_MAX_DEPTH) return DAS_ERR_SHAPE;
   if (c->num_layers < 1 || c->num_kv_heads < 1 || c->num_pages < 1) return DAS_ERR_SHAPE;
@@ -36,6 +39,8 @@ das_status check_cache(const das_cache *c) {
 das_status check_batch(const das_batch *b) {
   if (!b) return DAS_ERR_NULL;
   if (!b->prefix_len || !b->block_table) return DAS_ERR_NULL;
+  if (!aligned(b->prefix_len, 4) || !aligned(b->block_table, 4) || !aligned(b->dev_error, 4))
+    return DAS_ERR_ALIGN;
   if (b->batch < 1 || b->max_pages_per_seq < 1) return DAS_ERR_SHAPE;
   return DAS_OK;
 }
@@ -106,6 +111,9 @@ das_status attn_common(const das_cache *c, const das_batch *b, int layer, int ka
   st = check_batch(b);
   if (st != DAS_OK) return st;
   if (!q || !kb || !vb || !out) return DAS_ERR_NULL;
+  if (!aligned(q, 16) || !aligned(kb, 16) || !aligned(vb, 16) || !aligned(out, 16) ||
+      !aligned(lse, 4))
+    return DAS_ERR_ALIGN;
   if (layer < 0 || layer >= c->num_layers) return DAS_ERR_SHAPE;
   if (kappa < 1 || kappa > c->num_depths || nu < 1 || nu > c->num_depths) return DAS_ERR_DEPTH;
   const int kplane = c->k_plane[kappa];
@@ -219,6 +227,9 @@ das_status das_kv_append(const das_cache *cache, const das_batch *batch, const v
   st = check_batch(batch);
   if (st != DAS_OK) return st;
   if (!k_new || !v_new || !num_new) return DAS_ERR_NULL;
+  if (!aligned(k_new, 16) || !aligned(v_new, 16) || !aligned(num_new, 4) ||
+      !aligned(len_out, 4))
+    return DAS_ERR_ALIGN;
   if (w_max < 1 || w_max > DAS_MAX_BLOCK) return DAS_ERR_SHAPE;
   if (len_out && static_cast<const void *>(len_out) ==
                      static_cast<const void *>(batch->prefix_len))
@@ -256,6 +267,7 @@ const char *das_status_string(das_status status) {
     case DAS_ERR_WORKSPACE: return "workspace missing, misaligned or too small";
     case DAS_ERR_HIP: return "a HIP kernel launch failed";
     case DAS_ERR_UNSUPPORTED: return "request not supported by this build";
+    case DAS_ERR_ALIGN: return "a device array is not aligned as required";
   }
   return "unknown status";
 }

@@ -20,7 +20,7 @@ if torch.cuda.device_count() > 0:
 lib_mod = pytest.importorskip("paper_2609_34538_amd._lib")
 from paper_2609_34538_amd._lib import (DasBatchC, DasCacheC, DasOptionsC, LIB, MAX_DEPTH)  # noqa: E402
 
-OK, NULL, SHAPE, DEPTH, DTYPE, WS, HIP, UNSUP = 0, -1, -2, -3, -4, -5, -6, -7
+OK, NULL, SHAPE, DEPTH, DTYPE, WS, HIP, UNSUP, ALIGN = 0, -1, -2, -3, -4, -5, -6, -7, -8
 FAKE = 0x100000  # never dereferenced: every call below fails validation first
 
 
@@ -89,7 +89,7 @@ def test_workspace_size_formula():
     ("dtype", 7, DTYPE), ("num_depths", 0, SHAPE), ("num_depths", MAX_DEPTH + 1, SHAPE),
     ("num_layers", 0, SHAPE), ("num_kv_heads", 0, SHAPE), ("head_dim", 80, SHAPE),
     ("num_pages", 0, SHAPE), ("num_k_planes", 0, SHAPE), ("k_pool", None, NULL),
-    ("v_pool", None, NULL),
+    ("v_pool", None, NULL), ("k_pool", FAKE + 8, ALIGN), ("v_pool", FAKE + 2, ALIGN),
 ])
 def test_bad_cache_rejected(field, value, code):
     c, b = make_cache(), make_batch()
@@ -106,7 +106,8 @@ def test_bad_plane_map_rejected():
 
 @pytest.mark.parametrize("field,value,code", [
     ("batch", 0, SHAPE), ("max_pages_per_seq", 0, SHAPE), ("prefix_len", None, NULL),
-    ("block_table", None, NULL),
+    ("block_table", None, NULL), ("prefix_len", FAKE + 2, ALIGN),
+    ("block_table", FAKE + 1, ALIGN), ("dev_error", FAKE + 2, ALIGN),
 ])
 def test_bad_batch_rejected(field, value, code):
     c, b = make_cache(), make_batch()
@@ -132,6 +133,8 @@ def test_attention_argument_checks():
     assert draft(c, b, ws=None, nbytes=n) == WS
     assert draft(c, b, ws=FAKE, nbytes=n - 1) == WS
     assert draft(c, b, ws=FAKE + 4, nbytes=n) == WS  # not 256-byte aligned
+    assert draft(c, b, q=FAKE + 8) == ALIGN  # rows move in 16-byte pieces
+    assert draft(c, b, ptrs=FAKE + 4) == ALIGN
     # V at the full depth must be stored for a Mature-V read
     c2 = make_cache(vd=(31,))
     assert draft(c2, b, ws=FAKE, nbytes=n) == DEPTH
@@ -166,6 +169,10 @@ def test_append_argument_checks():
     assert app(w=0) == SHAPE
     assert app(w=65) == SHAPE
     assert app(lo=FAKE) == SHAPE  # len_out aliases prefix_len
+    assert app(k=FAKE + 8) == ALIGN
+    assert app(v=FAKE + 4) == ALIGN
+    assert app(n=FAKE + 2) == ALIGN
+    assert app(lo=FAKE + 0x1002) == ALIGN
     bad = make_cache()
     bad.head_dim = 100
     assert app(cc=bad) == SHAPE
