@@ -13,66 +13,87 @@ namespace das {
 namespace {
 
 constexpr int kRowsPerBlock = 8;
+constexpr int kEager = 16;  // splits whose partials are loaded before the count is known
 
-// One workgroup per (sequence, KV head, group of 8 rows). Each thread owns
-// (row, column) outputs and issues the loads of every split's (m, l, O)
-// together, so the merge costs one memory round trip.
+// One workgroup per (sequence, KV head, group of 8 rows); one thread per
+// (row, 4 consecutive columns). The partials of the first 16 splits that the
+// workspace can hold are loaded together with the prefix length, so a merge
+// of up to 16 splits costs one memory round trip; values of splits past the
+// sequence's count are discarded by selection, never used in arithmetic.
 template <typename T, int DH>
-__global__ __launch_bounds__(256) void attn_combine_kernel(AttnParams p, int skip_single) {
+__global__ __launch_bounds__(kRowsPerBlock * DH / 4) void attn_combine_kernel(AttnParams p,
+                                                                              int skip_single) {
   const int unit = blockIdx.x;  // b * hkv + kvh
   const int b = unit / p.hkv;
   const int kvh = unit % p.hkv;
+  const int row = blockIdx.y * kRowsPerBlock + threadIdx.x / (DH / 4);
+  const int c = 4 * (threadIdx.x % (DH / 4));
+  const bool live = row < p.rows;
+  const size_t base_row = (static_cast<size_t>(unit) * p.nsplit) * p.rows + (live ? row : 0);
+
+  const int s_raw = p.prefix_len[b];
+  float mv[kEager], lv[kEager];
+  float4 ov[kEager];
+#pragma unroll
+  for (int k = 0; k < kEager; ++k) {
+    const size_t r = base_row + static_cast<size_t>(k < p.nsplit ? k : 0) * p.rows;
+    mv[k] = p.ws_m[r];
+    lv[k] = p.ws_l[r];
+    ov[k] = *reinterpret_cast<const float4 *>(p.ws_o + r * DH + c);
+  }
   bool bad;
-  const int S = clamp_prefix(p.prefix_len[b], p.max_pages, &bad);
+  const int S = clamp_prefix(s_raw, p.max_pages, &bad);
   const int npages = (S + kPage - 1) / kPage;
   int ns = (npages + p.pages_per_split - 1) / p.pages_per_split;
   if (ns < 1) ns = 1;
-  if (ns == 1 && skip_single) return;  // the attention kernel wrote it
-  const size_t base_row = (static_cast<size_t>(unit) * p.nsplit) * p.rows;
-  T *out = static_cast<T *>(p.out);
-  const int row0 = blockIdx.y * kRowsPerBlock;
-  const int nrows = min(kRowsPerBlock, p.rows - row0);
+  if ((ns == 1 && skip_single) || !live) return;  // single split: the attention kernel wrote it
 
-  for (int e = threadIdx.x; e < nrows * DH; e += blockDim.x) {
-    const int row = row0 + e / DH, c = e % DH;
-    float mx = -__builtin_huge_valf(), num = 0.f, den = 0.f;
-    constexpr int CH = 8;
-    for (int s0 = 0; s0 < ns; s0 += CH) {
-      float mv[CH], lv[CH], ov[CH];
+  float mx = -__builtin_huge_valf();
 #pragma unroll
-      for (int k = 0; k < CH; ++k) {
-        const int s = s0 + k;
-        const size_t r = base_row + static_cast<size_t>(s < ns ? s : 0) * p.rows + row;
-        mv[k] = s < ns ? p.ws_m[r] : -__builtin_huge_valf();
-        lv[k] = p.ws_l[r];
-        ov[k] = p.ws_o[r * DH + c];
-      }
-      float cm = mx;
+  for (int k = 0; k < kEager; ++k) mx = k < ns ? fmaxf(mx, mv[k]) : mx;
+  float den = 0.f, n0 = 0.f, n1 = 0.f, n2 = 0.f, n3 = 0.f;
 #pragma unroll
-      for (int k = 0; k < CH; ++k) cm = fmaxf(cm, mv[k]);
-      const float rescale = exp2f(mx - cm);  // 0 on the first chunk (mx = -inf)
-      num *= rescale;
-      den *= rescale;
-#pragma unroll
-      for (int k = 0; k < CH; ++k) {
-        const float sc = exp2f(mv[k] - cm);
-        num += sc * ov[k];
-        den += sc * lv[k];
-      }
-      mx = cm;
+  for (int k = 0; k < kEager; ++k) {
+    if (k < ns) {
+      const float sc = exp2f(mv[k] - mx);
+      den += sc * lv[k];
+      n0 += sc * ov[k].x;
+      n1 += sc * ov[k].y;
+      n2 += sc * ov[k].z;
+      n3 += sc * ov[k].w;
     }
-    const int i = row / p.group, g = row % p.group;
-    const int h = kvh * p.group + g;
-    out[((static_cast<size_t>(b) * p.w + i) * p.hq + h) * DH + c] = from_f32<T>(num / den);
-    if (p.lse && c == 0)
-      p.lse[(static_cast<size_t>(b) * p.hq + h) * p.w + i] = (mx + log2f(den)) * 0.69314718055994530942f;
   }
+  // splits beyond the first 16, merged in the same online form
+  for (int s0 = kEager; s0 < ns; ++s0) {
+    const size_t r = base_row + static_cast<size_t>(s0) * p.rows;
+    const float m = p.ws_m[r], l = p.ws_l[r];
+    const float4 o = *reinterpret_cast<const float4 *>(p.ws_o + r * DH + c);
+    const float nm = fmaxf(mx, m);
+    const float a = exp2f(mx - nm), sc = exp2f(m - nm);
+    den = den * a + sc * l;
+    n0 = n0 * a + sc * o.x;
+    n1 = n1 * a + sc * o.y;
+    n2 = n2 * a + sc * o.z;
+    n3 = n3 * a + sc * o.w;
+    mx = nm;
+  }
+  const int i = row / p.group, g = row % p.group;
+  const int h = kvh * p.group + g;
+  T *out = static_cast<T *>(p.out) + ((static_cast<size_t>(b) * p.w + i) * p.hq + h) * DH + c;
+  const float inv = 1.f / den;
+  out[0] = from_f32<T>(n0 * inv);
+  out[1] = from_f32<T>(n1 * inv);
+  out[2] = from_f32<T>(n2 * inv);
+  out[3] = from_f32<T>(n3 * inv);
+  if (p.lse && c == 0)
+    p.lse[(static_cast<size_t>(b) * p.hq + h) * p.w + i] = (mx + log2f(den)) * 0.69314718055994530942f;
 }
 
 template <typename T, int DH>
 hipError_t launch_typed(const AttnParams &p, int skip_single, hipStream_t s) {
   dim3 grid(p.batch * p.hkv, (p.rows + kRowsPerBlock - 1) / kRowsPerBlock);
-  hipLaunchKernelGGL((attn_combine_kernel<T, DH>), grid, dim3(256), 0, s, p, skip_single);
+  hipLaunchKernelGGL((attn_combine_kernel<T, DH>), grid, dim3(kRowsPerBlock * DH / 4), 0, s, p,
+                     skip_single);
   return hipGetLastError();
 }
 

@@ -201,7 +201,11 @@ struct SeqBlock {
 // Fields of a decoded chunk, lane 8j + f of the descriptor register.
 enum { F_B = 0, F_KVH, F_RT, F_SPLIT, F_PG0, F_NPG, F_S, F_NSB };
 
-template <int DH, int NQ, int NB>
+// DIRECT: one workgroup per chunk (grid = every possible chunk, n_workers =
+// grid size); the chunk is decoded from the workgroup id, so the prefix
+// length, the chunk's page ids and its Q rows are fetched in one round trip.
+// Otherwise persistent workers scan the prefix lengths and walk their chunks.
+template <int DH, int NQ, int NB, bool DIRECT>
 __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, int n_workers) {
   using G = Geo<DH, NQ, NB>;
   constexpr int KS = G::KS;
@@ -251,6 +255,8 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, i
   };
 
   int totF = 0, totP = 0;
+  int my_chunks = 1;
+  if constexpr (!DIRECT) {
   for (int k = 0; k < nblocks; ++k) {
     load_block(k);
     const int bf = __shfl(sb.inclF, 63, 64), bp = __shfl(sb.inclP, 63, 64);
@@ -262,8 +268,9 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, i
     totP += bp;
   }
   const int total = totF + totP;
-  const int my_chunks = rank < total ? (total - rank + n_workers - 1) / n_workers : 0;
+  my_chunks = rank < total ? (total - rank + n_workers - 1) / n_workers : 0;
   if (my_chunks == 0) return;
+  }
 
   // Batch of decoded chunks: descv lane 8j + f = field f of chunk j, and
   // pid[j][i] = page id of the chunk's i-th page. The descriptors are
@@ -517,7 +524,63 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, i
     for (int k = 0; k < NB; ++k) try_issue();
   };
 
-  start_batch();
+  if constexpr (DIRECT) {
+    // chunk number -> (split group, row tile) as in the persistent order;
+    // group = (b * nsplit + split) * hkv + kvh
+    int grp, rt;
+    {
+      const int c = blockIdx.x, span = 8 * n_rt, runs = (n_workers / n_rt) >> 3;
+      if (c < runs * span) {
+        grp = 8 * (c / span) + (c % span & 7);
+        rt = (c % span) >> 3;
+      } else {
+        grp = c / n_rt;
+        rt = c % n_rt;
+      }
+    }
+    const int kvh = grp % p.hkv;
+    const int split = (grp / p.hkv) % p.nsplit;
+    const int b = grp / p.hkv / p.nsplit;
+    const int pg0 = split * pps;
+    // one round trip: prefix length, this split's page ids, Q rows
+    const int s_raw = p.prefix_len[b];
+    int page = 0;
+    if (lane < pps && pg0 + lane < p.max_pages)
+      page = p.block_table[static_cast<size_t>(b) * p.max_pages + pg0 + lane];
+    issue_q(0, b, kvh, rt);
+    bool bad;
+    const int S = clamp_prefix(s_raw, p.max_pages, &bad);
+    if (bad && split == 0 && kvh == 0 && rt == 0 && lane == 0)
+      report_error(p.dev_error, DAS_DEVERR_PREFIX);
+    const int npages = (S + kPage - 1) / kPage;
+    const int nsb = max(1, (npages + pps - 1) / pps);
+    if (split >= nsb) {
+      wait_vmcnt<0>();  // the Q rows land in LDS before the workgroup ends
+      return;
+    }
+    const int npg = max(0, min(pps, npages - pg0));
+    descv = lane == F_B ? b : descv;
+    descv = lane == F_KVH ? kvh : descv;
+    descv = lane == F_RT ? rt : descv;
+    descv = lane == F_SPLIT ? split : descv;
+    descv = lane == F_PG0 ? pg0 : descv;
+    descv = lane == F_NPG ? npg : descv;
+    descv = lane == F_S ? S : descv;
+    descv = lane == F_NSB ? nsb : descv;
+    pid[0][lane] = page;
+    batch_len = 1;
+    ij = 0;
+    it = 0;
+    cj = 0;
+    i_b = b;
+    i_kvh = kvh;
+    i_npg2 = 2 * npg;
+    i_ntile = i_npg2 + (split == 0 ? nblk : 0);
+    i_pages = page;
+    for (int k = 0; k < NB; ++k) try_issue();
+  } else {
+    start_batch();
+  }
   while (true) {
     if (cj >= batch_len) {
       batch_base += batch_len;
@@ -643,28 +706,35 @@ constexpr int workers_per_cu() {
 }
 
 template <int DH, int NQ, int NB>
-hipError_t launch_typed(const AttnParams &p, int n_cu, hipStream_t s) {
+hipError_t launch_typed(const AttnParams &p, int n_cu, int sched, hipStream_t s) {
   const int n_rt = (p.rows + 16 * NQ - 1) / (16 * NQ);
   const int workers = n_cu * workers_per_cu<DH, NQ, NB>();
-  hipLaunchKernelGGL((attn_mfma_kernel<DH, NQ, NB>), dim3(workers), dim3(64), 0, s, p, n_rt,
-                     workers);
+  // every possible chunk (the table width bounds the splits of a sequence)
+  const long slots = static_cast<long>(p.batch) * p.hkv * p.nsplit * n_rt;
+  const bool per_chunk =
+      sched == DAS_SCHED_PER_CHUNK || (sched == DAS_SCHED_AUTO && slots <= workers);
+  if (per_chunk) {
+    hipLaunchKernelGGL((attn_mfma_kernel<DH, NQ, NB, true>), dim3(static_cast<int>(slots)),
+                       dim3(64), 0, s, p, n_rt, static_cast<int>(slots));
+  } else {
+    hipLaunchKernelGGL((attn_mfma_kernel<DH, NQ, NB, false>), dim3(workers), dim3(64), 0, s, p,
+                       n_rt, workers);
+  }
   return hipGetLastError();
 }
 
 template <int DH>
-hipError_t launch_dh(const AttnParams &p, int n_cu, hipStream_t s) {
-  if (p.rows <= 16) return launch_typed<DH, 1, 2>(p, n_cu, s);
-  return launch_typed<DH, 2, 2>(p, n_cu, s);
+hipError_t launch_dh(const AttnParams &p, int n_cu, int sched, hipStream_t s) {
+  if (p.rows <= 16) return launch_typed<DH, 1, 2>(p, n_cu, sched, s);
+  return launch_typed<DH, 2, 2>(p, n_cu, sched, s);
 }
 
 }  // namespace
 
-int mfma_rows_per_wg(int rows) { return rows <= 16 ? 16 : 32; }
-
 // Compute units of each device, queried once (0 = not yet known).
 std::atomic<int> g_cu_count[kMaxDevices];
 
-hipError_t launch_attn_mfma(const AttnParams &p, int dh, hipStream_t s) {
+hipError_t launch_attn_mfma(const AttnParams &p, int dh, int sched, hipStream_t s) {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0) return hipErrorInvalidDevice;
   int n_cu = dev < kMaxDevices ? g_cu_count[dev].load(std::memory_order_relaxed) : 0;
@@ -675,9 +745,9 @@ hipError_t launch_attn_mfma(const AttnParams &p, int dh, hipStream_t s) {
     n_cu = (n_cu + 7) / 8 * 8;  // the worker ranking assumes a multiple of 8
     if (dev < kMaxDevices) g_cu_count[dev].store(n_cu, std::memory_order_relaxed);
   }
-  if (dh == 64) return launch_dh<64>(p, n_cu, s);
-  if (dh == 96) return launch_dh<96>(p, n_cu, s);
-  return launch_dh<128>(p, n_cu, s);
+  if (dh == 64) return launch_dh<64>(p, n_cu, sched, s);
+  if (dh == 96) return launch_dh<96>(p, n_cu, sched, s);
+  return launch_dh<128>(p, n_cu, sched, s);
 }
 
 }  // namespace das

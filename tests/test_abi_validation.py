@@ -85,6 +85,30 @@ def test_workspace_size_formula():
     assert ws_bytes(c, b, opts=o) == al(per * dh * 4) + 2 * al(per * 4)
 
 
+def _nsplit_default(B, hkv, maxp, path=2, hq=None, w=8):
+    c, b = make_cache(hkv=hkv), make_batch(B=B, maxp=maxp)
+    hq = hkv if hq is None else hq
+    o = DasOptionsC()
+    o.path, o.pages_per_split = path, 0
+    per_split = B * hkv * w * (hq // hkv)  # rows of one split
+    n = ws_bytes(c, b, hq=hq, w=w, opts=o)
+    for ns in range(1, maxp + 1):
+        al = lambda x: (x + 255) // 256 * 256
+        if al(per_split * ns * 128 * 4) + 2 * al(per_split * ns * 4) == n:
+            return ns
+    raise AssertionError("no split count matches the workspace size")
+
+
+def test_default_split_rule():
+    # about 8 splits per (sequence, KV head), 16 below 64 of them, >= 4 pages (2 on VALU)
+    assert _nsplit_default(B=16, hkv=8, maxp=200) == 8     # pps 25
+    assert _nsplit_default(B=4, hkv=8, maxp=257) == 16     # pps 17
+    assert _nsplit_default(B=1, hkv=8, maxp=33) == 9       # pps 4 (minimum)
+    assert _nsplit_default(B=1, hkv=8, maxp=33, path=1) == 11  # pps 3 on VALU
+    assert _nsplit_default(B=1, hkv=8, maxp=16, path=1) == 8   # pps 2 (VALU minimum)
+    assert _nsplit_default(B=32, hkv=8, maxp=1000) == 16   # pps 125 capped at 64 (MFMA)
+
+
 @pytest.mark.parametrize("field,value,code", [
     ("dtype", 7, DTYPE), ("num_depths", 0, SHAPE), ("num_depths", MAX_DEPTH + 1, SHAPE),
     ("num_layers", 0, SHAPE), ("num_kv_heads", 0, SHAPE), ("head_dim", 80, SHAPE),
@@ -155,6 +179,12 @@ def test_verify_and_policy_checks():
     assert LIB.das_attn_policy(ctypes.byref(c), ctypes.byref(b), 0, 32, 32, 32, 8, FAKE, FAKE,
                                FAKE, FAKE, None, FAKE, 1 << 30, ctypes.byref(o), None) == SHAPE
     o.path, o.pages_per_split = 0, -1
+    assert LIB.das_attn_policy(ctypes.byref(c), ctypes.byref(b), 0, 32, 32, 32, 8, FAKE, FAKE,
+                               FAKE, FAKE, None, FAKE, 1 << 30, ctypes.byref(o), None) == SHAPE
+    o.pages_per_split, o.schedule = 0, 3
+    assert LIB.das_attn_policy(ctypes.byref(c), ctypes.byref(b), 0, 32, 32, 32, 8, FAKE, FAKE,
+                               FAKE, FAKE, None, FAKE, 1 << 30, ctypes.byref(o), None) == SHAPE
+    o.schedule = -1
     assert LIB.das_attn_policy(ctypes.byref(c), ctypes.byref(b), 0, 32, 32, 32, 8, FAKE, FAKE,
                                FAKE, FAKE, None, FAKE, 1 << 30, ctypes.byref(o), None) == SHAPE
 

@@ -190,7 +190,7 @@ def _build_probe(path):
     return cd, q, kb, vb, targets, layer, d, lens
 
 
-@pytest.mark.parametrize("path", ["valu", "mfma"])
+@pytest.mark.parametrize("path", ["valu", "persistent", "per_chunk"])
 def test_onehot_probe_is_bit_exact(path):
     cd, q, kb, vb, targets, layer, d, lens = _build_probe(path)
     wl = cd.wl
@@ -199,7 +199,8 @@ def test_onehot_probe_is_bit_exact(path):
     err = torch.zeros(1, dtype=torch.int32, device=DEV)
     batch.dev_error = err
     batch.refresh()
-    out = das.attn_policy(cache, batch, layer, d, R, q, kb, vb, path=path, pages_per_split=1)
+    kind = dict(path="valu") if path == "valu" else dict(path="mfma", schedule=path)
+    out = das.attn_policy(cache, batch, layer, d, R, q, kb, vb, pages_per_split=1, **kind)
     torch.cuda.synchronize()
     got = out.float().cpu().numpy()
     assert int(err.item()) == 0

@@ -34,8 +34,14 @@ def small_workloads():
 EDGE_LENS = {"c3s": [0, 1, 63, 64, 65, 300]}
 
 
+# kernel family and (matrix-core) work schedule of a parametrised case
+KERNELS = {"valu": dict(path="valu"),
+           "mfma-persistent": dict(path="mfma", schedule="persistent"),
+           "mfma-per_chunk": dict(path="mfma", schedule="per_chunk")}
+
+
 def _paths(wl):
-    return ["valu"] if wl.dtype == torch.float32 else ["valu", "mfma"]
+    return ["valu"] if wl.dtype == torch.float32 else list(KERNELS)
 
 
 def _cases():
@@ -65,40 +71,41 @@ def test_draft_and_verify_match_oracle(small_data, name, path):
     for d, w in zip(wl.draft_depths, wl.draft_widths):
         q, kb, vb = dg.block_inputs(cd, w, d, DEV)
         lse = torch.empty((wl.batch, wl.hq, w), dtype=torch.float32, device=DEV)
-        out = das.attn_policy(cache, batch, layer, d, wl.depth_R, q, kb, vb, lse=lse, path=path)
+        out = das.attn_policy(cache, batch, layer, d, wl.depth_R, q, kb, vb, lse=lse,
+                              **KERNELS[path])
         torch.cuda.synchronize()
         ref, ref_lse = oracle_call(cd, layer, d, wl.depth_R, q, kb, vb, seqs)
         assert_close(out, ref, wl.dtype, f"{name} draft d={d} w={w} {path}")
         assert_lse_close(lse, ref_lse, f"{name} draft lse")
     q, kb, vb = dg.block_inputs(cd, wl.verify_width, wl.depth_R, DEV)
-    out = das.attn_policy(cache, batch, 0, wl.depth_R, wl.depth_R, q, kb, vb, path=path)
+    out = das.attn_policy(cache, batch, 0, wl.depth_R, wl.depth_R, q, kb, vb, **KERNELS[path])
     torch.cuda.synchronize()
     ref, _ = oracle_call(cd, 0, wl.depth_R, wl.depth_R, q, kb, vb, seqs)
     assert_close(out, ref, wl.dtype, f"{name} verify {path}")
 
 
-@pytest.mark.parametrize("path", ["valu", "mfma"])
+@pytest.mark.parametrize("path", list(KERNELS))
 @pytest.mark.parametrize("pps", [1, 2, 3, 100])
 def test_split_sizes_agree_with_oracle(small_data, path, pps):
     cd = small_data["c3s"]
     wl = cd.wl
     cache, batch = wrap(cd)
     q, kb, vb = dg.block_inputs(cd, 16, 2, DEV)
-    out = das.attn_policy(cache, batch, 1, 2, wl.depth_R, q, kb, vb, path=path,
-                          pages_per_split=pps)
+    out = das.attn_policy(cache, batch, 1, 2, wl.depth_R, q, kb, vb, pages_per_split=pps,
+                          **KERNELS[path])
     torch.cuda.synchronize()
     ref, _ = oracle_call(cd, 1, 2, wl.depth_R, q, kb, vb, range(wl.batch))
     assert_close(out, ref, wl.dtype, f"pps={pps} {path}")
 
 
-@pytest.mark.parametrize("path", ["valu", "mfma"])
+@pytest.mark.parametrize("path", list(KERNELS))
 @pytest.mark.parametrize("w", [1, 2, 3, 7, 17, 33, 64])
 def test_block_widths(small_data, w, path):
     cd = small_data["c5s"]
     wl = cd.wl
     cache, batch = wrap(cd)
     q, kb, vb = dg.block_inputs(cd, w, 3, DEV)
-    out = das.attn_policy(cache, batch, 0, 3, wl.depth_R, q, kb, vb, path=path)
+    out = das.attn_policy(cache, batch, 0, 3, wl.depth_R, q, kb, vb, **KERNELS[path])
     torch.cuda.synchronize()
     ref, _ = oracle_call(cd, 0, 3, wl.depth_R, q, kb, vb, range(wl.batch))
     assert_close(out, ref, wl.dtype, f"w={w} {path}")
@@ -124,14 +131,14 @@ def test_entry_points_are_policy_corners(small_data):
     assert torch.equal(c.view(torch.int16), e.view(torch.int16))
 
 
-@pytest.mark.parametrize("path", ["valu", "mfma"])
+@pytest.mark.parametrize("path", list(KERNELS))
 def test_deterministic(small_data, path):
     cd = small_data["c4s"]
     wl = cd.wl
     cache, batch = wrap(cd)
     q, kb, vb = dg.block_inputs(cd, 32, 3, DEV)
-    a = das.attn_policy(cache, batch, 0, 3, wl.depth_R, q, kb, vb, path=path)
-    b = das.attn_policy(cache, batch, 0, 3, wl.depth_R, q, kb, vb, path=path)
+    a = das.attn_policy(cache, batch, 0, 3, wl.depth_R, q, kb, vb, **KERNELS[path])
+    b = das.attn_policy(cache, batch, 0, 3, wl.depth_R, q, kb, vb, **KERNELS[path])
     torch.cuda.synchronize()
     assert torch.equal(a.view(torch.int16), b.view(torch.int16)), path
 
@@ -151,15 +158,17 @@ def test_all_read_policies(small_data):
         assert_close(out, ref, wl.dtype, f"policy ({kappa},{nu})")
 
 
+@pytest.mark.parametrize("sched", ["persistent", "per_chunk"])
 @pytest.mark.parametrize("pps", [0, 63, 64, 100])
-def test_long_prefix_split_sizes(pps):
+def test_long_prefix_split_sizes(pps, sched):
     """Splits longer than 64 pages are clamped; a 5000-token prefix spans 79
     pages, so every clamp and the last partial split are exercised."""
     wl = dg.scaled(W[5], batch=3, hq=2, hkv=2, layers=1, prefix=(4000, 5000))
     cd = dg.make_cache(wl, DEV, prefix_lens=[5000, 4100, 64 * 64])
     cache, batch = wrap(cd)
     q, kb, vb = dg.block_inputs(cd, 16, 2, DEV)
-    out = das.attn_policy(cache, batch, 0, 2, wl.depth_R, q, kb, vb, pages_per_split=pps)
+    out = das.attn_policy(cache, batch, 0, 2, wl.depth_R, q, kb, vb, pages_per_split=pps,
+                          schedule=sched)
     torch.cuda.synchronize()
     ref, _ = oracle_call(cd, 0, 2, wl.depth_R, q, kb, vb, range(wl.batch))
     assert_close(out, ref, wl.dtype, f"long prefix pps={pps}")
