@@ -94,12 +94,17 @@ typedef enum das_dtype { DAS_F32 = 0, DAS_BF16 = 1 } das_dtype;
  * sequence's logical page p is the physical page block_table[b][p], the same
  * physical page in every plane, layer and head.
  *
- *   k_pool: [num_k_planes][L][Hkv][num_pages][64][head_dim]  token-major pages
- *   v_pool: [num_v_planes][L][Hkv][num_pages][head_dim][64]  dim-major pages
+ *   k_pool: [num_k_planes][L][Hkv][num_pages][64][head_dim]     token-major
+ *   v_pool: [num_v_planes][L][Hkv][num_pages][8][head_dim][8]   token-grouped
  *
- * Keys are stored token-major and values dim-major so that both page tiles
- * are single contiguous blocks and feed the two matrix products (Q K^T and
- * P V) with their reduction dimension contiguous.
+ * Keys are stored token-major: position t of a page is row t. Values are
+ * stored in groups of 8 positions: position t of a page is element
+ * [t / 8][d][t % 8], so for every head dimension d the 8 positions of a
+ * group are 16 contiguous bytes (bf16). Both products then read their
+ * reduction dimension contiguously (Q K^T reduces over head_dim, P V over
+ * positions), any 8-aligned run of positions of the value page is one
+ * contiguous block, and a commit of 8 aligned positions writes one
+ * contiguous head_dim x 16-byte block per (plane, layer, head).
  *
  * k_plane[r] / v_plane[r] (r = 1..R) give the plane holding depth r, or -1
  * when that depth is not stored; entry 0 is unused. Only the depths that a

@@ -112,7 +112,7 @@ def _stream_handle(stream) -> int:
 class PagedCache:
     """Caller-owned depth-indexed paged cache (layouts as in das.h).
 
-    k_pool: [nK, L, Hkv, P, 64, dh]; v_pool: [nV, L, Hkv, P, dh, 64].
+    k_pool: [nK, L, Hkv, P, 64, dh]; v_pool: [nV, L, Hkv, P, 8, dh, 8].
     k_plane / v_plane map a depth r (1..R) to its plane index."""
     k_pool: torch.Tensor
     v_pool: torch.Tensor
@@ -146,11 +146,11 @@ class PagedCache:
 
     def refresh(self):
         k, v = self.k_pool, self.v_pool
-        if k.dim() != 6 or v.dim() != 6:
-            raise ValueError("pools must be 6-d")
-        if k.shape[4] != PAGE_TOKENS or v.shape[5] != PAGE_TOKENS:
-            raise ValueError("pages hold 64 tokens")
-        if k.shape[1:4] != v.shape[1:4] or k.shape[5] != v.shape[4] or k.dtype != v.dtype:
+        if k.dim() != 6 or v.dim() != 7:
+            raise ValueError("k_pool must be 6-d and v_pool 7-d")
+        if k.shape[4] != PAGE_TOKENS or v.shape[4] * v.shape[6] != PAGE_TOKENS or v.shape[6] != 8:
+            raise ValueError("pages hold 64 tokens (values in 8 groups of 8)")
+        if k.shape[1:4] != v.shape[1:4] or k.shape[5] != v.shape[5] or k.dtype != v.dtype:
             raise ValueError("k_pool / v_pool disagree")
         if not (k.is_contiguous() and v.is_contiguous()):
             raise ValueError("pools must be contiguous")

@@ -34,7 +34,8 @@
 // chosen so that the C fragments of the tile's two S^T halves hold, per lane,
 // the 8 consecutive tokens 8g .. 8g + 7; those are exactly the k slots of the
 // P^T fragment of the P.V product, and the matching V^T fragment is one
-// contiguous 16-byte load from the dim-major value page. The draft block's
+// contiguous 16-byte load from the token-grouped value page ([8][dh][8]);
+// a 32-token tile of that page is one contiguous block. The draft block's
 // values are token-major; their V^T fragments are gathered from LDS.
 //
 // A chunk ends by writing its (m, l, O) partial to the workspace for the
@@ -346,9 +347,10 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, i
   const size_t head_bytes = static_cast<size_t>(p.num_pages) * kPage * DH * 2;
   const size_t tok_bytes = static_cast<size_t>(p.hkv) * DH * 2;  // block row stride
   // per-lane byte offsets of the fragments inside a page: key token slot
-  // 8(n/4) + n%4 (plus a uniform part), column 8g; value row n, token 8g
+  // 8(n/4) + n%4 (plus a uniform part), column 8g; value token group g of
+  // the tile, head dim n
   const uint32_t lane_k = ((8 * (ln >> 2) + (ln & 3)) * DH + 8 * lg) * 2;
-  const uint32_t lane_v = (ln * kPage + 8 * lg) * 2;
+  const uint32_t lane_v = (lg * DH + ln) * 16;
 
   // Issue cursor: batch chunk ij, next tile it of its ntile (= 2 npg page
   // tiles, then nblk block tiles on split 0); n_issued tiles so far. Compute
@@ -392,7 +394,7 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, i
           const size_t off = i_kvh * head_bytes + static_cast<size_t>(ok ? page : 0) * kPage * DH * 2;
           const int u = it & 1;
           const char *kb = kl + off + (32 * u) * DH * 2;
-          const char *vb = vl + off + (32 * u) * 2;
+          const char *vb = vl + off + 64 * DH * u;  // token groups 4u .. 4u + 3
 #pragma unroll
           for (int e = 0; e < 2; ++e)
 #pragma unroll
@@ -400,7 +402,7 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, i
               dma16(kb + (4 * e * DH + 32 * ks) * 2 + lane_k, slot + (e * KS + ks) * kFragBytes);
 #pragma unroll
           for (int dt = 0; dt < DT; ++dt)
-            dma16(vb + (16 * dt * kPage) * 2 + lane_v, slot + (2 * KS + dt) * kFragBytes);
+            dma16(vb + 256 * dt + lane_v, slot + (2 * KS + dt) * kFragBytes);
         } else {
           // draft block tile u: key fragments by token slot, value rows raw
           const int u = it - i_npg2;
@@ -462,7 +464,7 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, i
           const size_t off = i_kvh * head_bytes + static_cast<size_t>(ok ? page : 0) * kPage * DH * 2;
           s_u = it & 1;
           s_kb = kl + off + (32 * s_u) * DH * 2;
-          s_vb = vl + off + (32 * s_u) * 2;
+          s_vb = vl + off + 64 * DH * s_u;
         } else {
           s_u = it - i_npg2;
           s_kb = static_cast<const char *>(p.kb) + (static_cast<size_t>(i_b) * p.w * p.hkv + i_kvh) * DH * 2;
@@ -500,7 +502,7 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, i
       if (!s_blk) {
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt)
-          dma16(s_vb + (16 * dt * kPage) * 2 + lane_v, s_slot + (2 * KS + dt) * kFragBytes);
+          dma16(s_vb + 256 * dt + lane_v, s_slot + (2 * KS + dt) * kFragBytes);
       } else {
 #pragma unroll
         for (int f = 0; f < DT; ++f) {

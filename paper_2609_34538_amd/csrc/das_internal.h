@@ -17,7 +17,7 @@ constexpr int kMaxPagesPerSplit = 64;   // matrix-core kernel: one page id per l
 // kernel only adds (kv head, page) offsets.
 struct AttnParams {
   const void *k_layer;   // [Hkv][P][64][dh]   keys of plane kappa, layer l
-  const void *v_layer;   // [Hkv][P][dh][64]   values of plane nu, layer l
+  const void *v_layer;   // [Hkv][P][8][dh][8] values of plane nu, layer l
   const void *q;         // [B][w][Hq][dh]
   const void *kb;        // [B][w][Hkv][dh]
   const void *vb;        // [B][w][Hkv][dh]
@@ -39,7 +39,7 @@ struct AppendParams {
   const void *k_new;     // [nK][L][B][w_max][Hkv][dh]
   const void *v_new;     // [nV][L][B][w_max][Hkv][dh]
   void *k_pool;          // [nK][L][Hkv][P][64][dh]
-  void *v_pool;          // [nV][L][Hkv][P][dh][64]
+  void *v_pool;          // [nV][L][Hkv][P][8][dh][8]
   const int32_t *prefix_len;
   const int32_t *block_table;
   const int32_t *num_new;

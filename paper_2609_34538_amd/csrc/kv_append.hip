@@ -10,8 +10,8 @@
 //  - keys: copies the n token rows with 16-byte vectors (rows of head_dim
 //    are contiguous in both the source and the token-major page);
 //  - values: stages up to 16 token rows in LDS and writes them into the
-//    dim-major page transposed, lanes walking the token index so a wave's
-//    writes are runs of consecutive positions.
+//    token-grouped page ([8][dh][8]) transposed, lanes walking the token
+//    index, so a wave's writes are runs of consecutive 16-byte groups.
 // Pure copies: results are bit-exact.
 
 #include "das_internal.h"
@@ -127,7 +127,7 @@ __global__ __launch_bounds__(64 * kWaves) void kv_append_kernel(AppendParams p) 
         const bool second = pos / kPage != first_page;
         if (second ? ok1 : ok0) {
           const size_t page = second ? pg1 : pg0;
-          dst[(page * DH + c) * kPage + pos % kPage] = st[t * DH + c];
+          dst[page * kPage * DH + ((pos % kPage) / 8 * DH + c) * 8 + pos % 8] = st[t * DH + c];
         }
       }
     }

@@ -112,7 +112,7 @@ class CacheData:
     block_table: np.ndarray            # [B, max_pages] int32 (-1 = unused)
     pages_of: List[np.ndarray]         # physical pages of each sequence, in order
     k_pool: torch.Tensor               # [nK, L, Hkv, P, 64, dh]
-    v_pool: torch.Tensor               # [nV, L, Hkv, P, dh, 64]
+    v_pool: torch.Tensor               # [nV, L, Hkv, P, 8, dh, 8]
     k_plane: Dict[int, int]
     v_plane: Dict[int, int]
     gen: torch.Generator = field(repr=False, default=None)
@@ -164,8 +164,8 @@ def make_cache(wl: Workload, device="cuda", prefix_lens: Optional[Sequence[int]]
     gen.manual_seed(wl.seed)
     shape = (wl.hkv, total, PAGE, wl.dh)
     k_pool = torch.empty((len(kd), wl.layers) + shape, dtype=wl.dtype, device=device)
-    v_pool = torch.empty((len(vd), wl.layers, wl.hkv, total, wl.dh, PAGE), dtype=wl.dtype,
-                         device=device)
+    v_pool = torch.empty((len(vd), wl.layers, wl.hkv, total, PAGE // 8, wl.dh, 8),
+                         dtype=wl.dtype, device=device)
     for layer in range(wl.layers):
         for pool, depths, is_v in ((k_pool, kd, False), (v_pool, vd, True)):
             cur = torch.randn(shape, generator=gen, device=device, dtype=torch.float32)
@@ -178,8 +178,9 @@ def make_cache(wl: Workload, device="cuda", prefix_lens: Optional[Sequence[int]]
                 x = cur
                 if wl.k_gain is not None and not is_v:
                     x = cur * (wl.k_gain / depth_std(wl, d))
-                if is_v:
-                    pool[i, layer].copy_(x.transpose(-1, -2))
+                if is_v:  # token-grouped value pages [8][dh][8]
+                    pool[i, layer].copy_(
+                        x.reshape(wl.hkv, total, PAGE // 8, 8, wl.dh).transpose(-1, -2))
                 else:
                     pool[i, layer].copy_(x)
             del cur
@@ -241,6 +242,6 @@ def gather_prefix_v(cd: CacheData, b: int, plane: int, layer: int, s_len: int,
     table = cd.block_table if table is None else table
     npg = -(-s_len // PAGE)
     pages = torch.as_tensor(table[b, :npg].astype(np.int64), device=cd.v_pool.device)
-    t = cd.v_pool[plane, layer].index_select(1, pages)         # [Hkv, npg, dh, 64]
-    t = t.permute(1, 3, 0, 2).reshape(npg * PAGE, cd.wl.hkv, cd.wl.dh)[:s_len]
+    t = cd.v_pool[plane, layer].index_select(1, pages)         # [Hkv, npg, 8, dh, 8]
+    t = t.permute(1, 2, 4, 0, 3).reshape(npg * PAGE, cd.wl.hkv, cd.wl.dh)[:s_len]
     return t.double().cpu().numpy()

@@ -3,8 +3,9 @@ that pin page-table resolution, key/value plane selection, core layer, GQA
 head map, the prefix-length boundary and the in-block causal mask.
 
 The probes write the cache directly with the layout documented in das.h
-(physical page block_table[b][pos // 64], row pos % 64; keys token-major,
-values dim-major), independently of the test data generator."""
+(physical page block_table[b][pos // 64], slot pos % 64; keys token-major
+[slot][dh], values token-grouped [slot // 8][dh][slot % 8]), independently of
+the test data generator."""
 
 from __future__ import annotations
 
@@ -32,7 +33,7 @@ def _expected_after_append(cd, k_before, v_before, k_new, v_new, lens, num_new):
             pos = s + t
             page = int(cd.block_table[b, pos // 64])
             k_exp[:, :, :, page, pos % 64, :] = k_new[:, :, b, t, :, :]
-            v_exp[:, :, :, page, :, pos % 64] = v_new[:, :, b, t, :, :]
+            v_exp[:, :, :, page, (pos % 64) // 8, :, pos % 8] = v_new[:, :, b, t, :, :]
     return k_exp, v_exp
 
 
@@ -146,7 +147,7 @@ def _build_probe(path):
                 for r, p in cd.v_plane.items():
                     for layer in range(wl.layers):
                         for h in range(wl.hkv):
-                            v[p, layer, h, page, :5, slot] = torch.tensor(
+                            v[p, layer, h, page, slot // 8, :5, slot % 8] = torch.tensor(
                                 _code(pos, r, layer, h), dtype=v.dtype)
     # every query row (b, i, h) targets its own coordinate c = i * G + h % G
     # and the prefix position hot[b][g][c] whose key at depth d holds e_c;
