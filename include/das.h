@@ -147,23 +147,11 @@ typedef enum das_attn_path {
   DAS_PATH_MFMA = 2   /* matrix-core kernel (bf16 only)                      */
 } das_attn_path;
 
-/* How the matrix-core kernel maps work to workgroups (das_attn_options). */
-typedef enum das_attn_schedule {
-  DAS_SCHED_AUTO = 0,        /* per-chunk when every chunk fits one pass of the
-                                persistent workers, persistent otherwise         */
-  DAS_SCHED_PERSISTENT = 1,  /* one worker per resident wave slot; workers scan
-                                the prefix lengths and take chunks round-robin   */
-  DAS_SCHED_PER_CHUNK = 2    /* one workgroup per possible chunk of the table
-                                width; empty chunks exit at once                 */
-} das_attn_schedule;
-
 typedef struct das_attn_options {
   int32_t path;             /* das_attn_path                                 */
   int32_t pages_per_split;  /* prefix pages per split; 0 = library choice;
                                clamped to the block table width, and to 64
                                on the matrix-core path                       */
-  int32_t schedule;         /* das_attn_schedule; ignored on the vector-ALU
-                               path                                          */
 } das_attn_options;
 
 /*

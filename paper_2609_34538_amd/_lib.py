@@ -31,7 +31,6 @@ STATUS_NAMES = {0: "DAS_OK", -1: "DAS_ERR_NULL", -2: "DAS_ERR_SHAPE", -3: "DAS_E
                 -7: "DAS_ERR_UNSUPPORTED", -8: "DAS_ERR_ALIGN"}
 DTYPE_CODES = {torch.float32: 0, torch.bfloat16: 1}
 PATHS = {"auto": 0, "valu": 1, "mfma": 2}
-SCHEDULES = {"auto": 0, "persistent": 1, "per_chunk": 2}
 DEVERR_PAGE, DEVERR_PREFIX, DEVERR_COMMIT = 1, 2, 4
 
 EXPORTED = ["das_attn_workspace_bytes", "das_attn_workspace_bytes_ex", "das_attn_draft_maturev",
@@ -59,7 +58,7 @@ class DasBatchC(ctypes.Structure):
 
 
 class DasOptionsC(ctypes.Structure):
-    _fields_ = [("path", c_int32), ("pages_per_split", c_int32), ("schedule", c_int32)]
+    _fields_ = [("path", c_int32), ("pages_per_split", c_int32)]
 
 
 def _load() -> ctypes.CDLL:
@@ -208,11 +207,10 @@ class Batch:
         return self._c
 
 
-def _options(path: str, pages_per_split: int, schedule: str = "auto"):
+def _options(path: str, pages_per_split: int):
     o = DasOptionsC()
     o.path = PATHS[path]
     o.pages_per_split = pages_per_split
-    o.schedule = SCHEDULES[schedule]
     return o
 
 
@@ -248,14 +246,14 @@ def attn_policy(cache: PagedCache, batch: Batch, layer: int, kappa: int, nu: int
                 q: torch.Tensor, k_blk: torch.Tensor, v_blk: torch.Tensor,
                 out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
                 workspace: Optional[torch.Tensor] = None, path: str = "auto",
-                pages_per_split: int = 0, stream=None, schedule: str = "auto") -> torch.Tensor:
+                pages_per_split: int = 0, stream=None) -> torch.Tensor:
     """Eq. (2)-(3) with prefix keys at depth kappa and values at depth nu."""
     w, hq = _check_block(cache, batch, q, k_blk, v_blk)
     if out is None:
         out = torch.empty_like(q)
     if workspace is None:
         workspace = alloc_workspace(cache, batch, hq, w, path, pages_per_split)
-    o = _options(path, pages_per_split, schedule)
+    o = _options(path, pages_per_split)
     st = LIB.das_attn_policy(ctypes.byref(cache.c), ctypes.byref(batch.c), layer, kappa, nu,
                              hq, w, q.data_ptr(), k_blk.data_ptr(), v_blk.data_ptr(),
                              out.data_ptr(), _ptr(lse), workspace.data_ptr(),
@@ -273,13 +271,12 @@ class PreparedAttention:
     def __init__(self, cache: PagedCache, batch: Batch, layer: int, kappa: int, nu: int,
                  q: torch.Tensor, k_blk: torch.Tensor, v_blk: torch.Tensor,
                  out: torch.Tensor, workspace: torch.Tensor, lse: Optional[torch.Tensor] = None,
-                 path: str = "auto", pages_per_split: int = 0, stream=None,
-                 schedule: str = "auto"):
+                 path: str = "auto", pages_per_split: int = 0, stream=None):
         w, hq = _check_block(cache, batch, q, k_blk, v_blk)
         if out.shape != q.shape or out.dtype != q.dtype or not out.is_contiguous():
             raise ValueError("out must match q")
         self._keep = (cache, batch, q, k_blk, v_blk, out, workspace, lse)
-        self._opts = _options(path, pages_per_split, schedule)
+        self._opts = _options(path, pages_per_split)
         self._fn = LIB.das_attn_policy
         self._args = (ctypes.byref(cache.c), ctypes.byref(batch.c), layer, kappa, nu, hq, w,
                       q.data_ptr(), k_blk.data_ptr(), v_blk.data_ptr(), out.data_ptr(),

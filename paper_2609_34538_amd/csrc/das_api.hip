@@ -62,22 +62,21 @@ struct Plan {
 };
 
 // Prefix pages of one sequence are cut into splits of pages_per_split pages;
-// each (split, KV head, row tile) is one chunk of work. The default cuts each
-// (sequence, KV head) into about 8 splits, 16 when there are fewer than 64
-// of them, at least 4 pages each (2 on the vector-ALU path): enough chunks
-// for the persistent workers to balance while every split still streams
-// several pages per partial result it writes. (Measured on MI355X over 1, 2,
-// 3, 4, 8, 16, 32, 64 pages per split on the single-sequence, ragged,
-// long-prefix and wave-step workloads; this rule picks the best or within
-// 2 % of it on each.)
+// each (split, KV head, row tile) is one chunk of work, one workgroup on the
+// matrix-core path. The default cuts each (sequence, KV head) into at least
+// 8 splits, 16 when there are fewer than 64 (sequence, KV head) pairs, of at
+// least 2 pages: enough workgroups to keep every compute unit streaming
+// while each split still covers several pages per partial result it writes.
+// (Measured on MI355X over 1, 2, 3, 4, 6, 8, 16, 32, 64 pages per split on
+// the single-sequence, ragged, long-prefix and wave-step workloads; this
+// rule picks the best or within 1 % of it on each.)
 das_status make_plan(const das_cache *c, const das_batch *b, int hq, int w,
                      const das_attn_options *o, Plan *plan) {
   if (hq < 1 || hq % c->num_kv_heads != 0) return DAS_ERR_SHAPE;
   const int group = hq / c->num_kv_heads;
   if (group > 8) return DAS_ERR_UNSUPPORTED;
   if (w < 1 || w > DAS_MAX_BLOCK) return DAS_ERR_SHAPE;
-  if (o && (o->pages_per_split < 0 || o->path < DAS_PATH_AUTO || o->path > DAS_PATH_MFMA ||
-            o->schedule < DAS_SCHED_AUTO || o->schedule > DAS_SCHED_PER_CHUNK))
+  if (o && (o->pages_per_split < 0 || o->path < DAS_PATH_AUTO || o->path > DAS_PATH_MFMA))
     return DAS_ERR_SHAPE;
   if (o && o->path == DAS_PATH_MFMA && c->dtype != DAS_BF16) return DAS_ERR_UNSUPPORTED;
   plan->path = choose_path(c, o);
@@ -87,9 +86,8 @@ das_status make_plan(const das_cache *c, const das_batch *b, int hq, int w,
   if (pps == 0) {
     const long seq_heads = static_cast<long>(b->batch) * c->num_kv_heads;
     const long splits = seq_heads < 64 ? 16 : 8;
-    long want = (maxp + splits - 1) / splits;
-    const long min_pps = plan->path == DAS_PATH_MFMA ? 4 : 2;
-    if (want < min_pps) want = min_pps;
+    long want = maxp / splits;
+    if (want < 2) want = 2;
     pps = static_cast<int>(want);
   }
   if (pps > maxp) pps = maxp;
@@ -162,8 +160,7 @@ das_status attn_common(const das_cache *c, const das_batch *b, int layer, int ka
   p.scale_log2 = static_cast<float>(log2e / __builtin_sqrt(static_cast<double>(dh)));
 
   const bool mfma = plan.path == DAS_PATH_MFMA;
-  const int sched = o ? o->schedule : DAS_SCHED_AUTO;
-  const hipError_t e = mfma ? launch_attn_mfma(p, dh, sched, stream)
+  const hipError_t e = mfma ? launch_attn_mfma(p, dh, stream)
                             : launch_attn_valu(p, c->dtype, dh, stream);
   if (e != hipSuccess) return DAS_ERR_HIP;
   if (launch_attn_combine(p, c->dtype, dh, mfma ? 1 : 0, stream) != hipSuccess) return DAS_ERR_HIP;

@@ -50,8 +50,7 @@ struct AppendParams {
 
 // Launchers (return the hipError_t of the launch).
 hipError_t launch_attn_valu(const AttnParams &p, int dtype, int dh, hipStream_t s);
-// sched: das_attn_schedule
-hipError_t launch_attn_mfma(const AttnParams &p, int dh, int sched, hipStream_t s);
+hipError_t launch_attn_mfma(const AttnParams &p, int dh, hipStream_t s);
 // skip_single: sequences whose prefix fits one split were already written
 // by the attention kernel (matrix-core path).
 hipError_t launch_attn_combine(const AttnParams &p, int dtype, int dh, int skip_single,

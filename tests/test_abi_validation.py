@@ -100,12 +100,12 @@ def _nsplit_default(B, hkv, maxp, path=2, hq=None, w=8):
 
 
 def test_default_split_rule():
-    # about 8 splits per (sequence, KV head), 16 below 64 of them, >= 4 pages (2 on VALU)
+    # pps = max(2, maxp // 8), maxp // 16 below 64 (sequence, KV head) pairs
     assert _nsplit_default(B=16, hkv=8, maxp=200) == 8     # pps 25
-    assert _nsplit_default(B=4, hkv=8, maxp=257) == 16     # pps 17
-    assert _nsplit_default(B=1, hkv=8, maxp=33) == 9       # pps 4 (minimum)
-    assert _nsplit_default(B=1, hkv=8, maxp=33, path=1) == 11  # pps 3 on VALU
-    assert _nsplit_default(B=1, hkv=8, maxp=16, path=1) == 8   # pps 2 (VALU minimum)
+    assert _nsplit_default(B=4, hkv=8, maxp=257) == 17     # pps 16
+    assert _nsplit_default(B=1, hkv=55, maxp=33) == 17     # pps 2
+    assert _nsplit_default(B=1, hkv=8, maxp=20) == 10      # pps 2 (minimum)
+    assert _nsplit_default(B=1, hkv=8, maxp=33, path=1) == 17  # same rule on VALU
     assert _nsplit_default(B=32, hkv=8, maxp=1000) == 16   # pps 125 capped at 64 (MFMA)
 
 
@@ -179,12 +179,6 @@ def test_verify_and_policy_checks():
     assert LIB.das_attn_policy(ctypes.byref(c), ctypes.byref(b), 0, 32, 32, 32, 8, FAKE, FAKE,
                                FAKE, FAKE, None, FAKE, 1 << 30, ctypes.byref(o), None) == SHAPE
     o.path, o.pages_per_split = 0, -1
-    assert LIB.das_attn_policy(ctypes.byref(c), ctypes.byref(b), 0, 32, 32, 32, 8, FAKE, FAKE,
-                               FAKE, FAKE, None, FAKE, 1 << 30, ctypes.byref(o), None) == SHAPE
-    o.pages_per_split, o.schedule = 0, 3
-    assert LIB.das_attn_policy(ctypes.byref(c), ctypes.byref(b), 0, 32, 32, 32, 8, FAKE, FAKE,
-                               FAKE, FAKE, None, FAKE, 1 << 30, ctypes.byref(o), None) == SHAPE
-    o.schedule = -1
     assert LIB.das_attn_policy(ctypes.byref(c), ctypes.byref(b), 0, 32, 32, 32, 8, FAKE, FAKE,
                                FAKE, FAKE, None, FAKE, 1 << 30, ctypes.byref(o), None) == SHAPE
 

@@ -191,7 +191,7 @@ def _build_probe(path):
     return cd, q, kb, vb, targets, layer, d, lens
 
 
-@pytest.mark.parametrize("path", ["valu", "persistent", "per_chunk"])
+@pytest.mark.parametrize("path", ["valu", "mfma"])
 def test_onehot_probe_is_bit_exact(path):
     cd, q, kb, vb, targets, layer, d, lens = _build_probe(path)
     wl = cd.wl
@@ -200,8 +200,7 @@ def test_onehot_probe_is_bit_exact(path):
     err = torch.zeros(1, dtype=torch.int32, device=DEV)
     batch.dev_error = err
     batch.refresh()
-    kind = dict(path="valu") if path == "valu" else dict(path="mfma", schedule=path)
-    out = das.attn_policy(cache, batch, layer, d, R, q, kb, vb, pages_per_split=1, **kind)
+    out = das.attn_policy(cache, batch, layer, d, R, q, kb, vb, path=path, pages_per_split=1)
     torch.cuda.synchronize()
     got = out.float().cpu().numpy()
     assert int(err.item()) == 0

@@ -34,10 +34,8 @@ def small_workloads():
 EDGE_LENS = {"c3s": [0, 1, 63, 64, 65, 300]}
 
 
-# kernel family and (matrix-core) work schedule of a parametrised case
-KERNELS = {"valu": dict(path="valu"),
-           "mfma-persistent": dict(path="mfma", schedule="persistent"),
-           "mfma-per_chunk": dict(path="mfma", schedule="per_chunk")}
+# kernel family of a parametrised case
+KERNELS = {"valu": dict(path="valu"), "mfma": dict(path="mfma")}
 
 
 def _paths(wl):
@@ -158,17 +156,15 @@ def test_all_read_policies(small_data):
         assert_close(out, ref, wl.dtype, f"policy ({kappa},{nu})")
 
 
-@pytest.mark.parametrize("sched", ["persistent", "per_chunk"])
 @pytest.mark.parametrize("pps", [0, 63, 64, 100])
-def test_long_prefix_split_sizes(pps, sched):
+def test_long_prefix_split_sizes(pps):
     """Splits longer than 64 pages are clamped; a 5000-token prefix spans 79
     pages, so every clamp and the last partial split are exercised."""
     wl = dg.scaled(W[5], batch=3, hq=2, hkv=2, layers=1, prefix=(4000, 5000))
     cd = dg.make_cache(wl, DEV, prefix_lens=[5000, 4100, 64 * 64])
     cache, batch = wrap(cd)
     q, kb, vb = dg.block_inputs(cd, 16, 2, DEV)
-    out = das.attn_policy(cache, batch, 0, 2, wl.depth_R, q, kb, vb, pages_per_split=pps,
-                          schedule=sched)
+    out = das.attn_policy(cache, batch, 0, 2, wl.depth_R, q, kb, vb, pages_per_split=pps)
     torch.cuda.synchronize()
     ref, _ = oracle_call(cd, 0, 2, wl.depth_R, q, kb, vb, range(wl.batch))
     assert_close(out, ref, wl.dtype, f"long prefix pps={pps}")
