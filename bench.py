@@ -10,12 +10,16 @@ Default workload: a single sequence shaped like the paper's looped models
 (bf16, 55 query = 55 KV heads, head_dim 96, verified prefix 2048, draft block
 8, R = 32, d = 4, 4 core layers, every depth of the cache stored).
 Successive steps rotate over disjoint copies of the cache pages so that the
-bytes a step reads are not served by the 256 MB last-level cache.
+bytes a step reads are not served by the 256 MB last-level cache. Each step
+is captured once per cache copy as a HIP graph and replayed (--eager launches
+every call from the host instead).
 
-Prints one JSON line: throughput (block tokens per second), the roofline of
-the dominant kernel (the attention launches, HBM bound, algorithmic bytes
-over their average duration measured with HIP events on their stream), and
-the fp64 oracle timed on the host's cores on a bounded sample.
+Prints one JSON line: throughput (block tokens per second, HIP events around
+the timed steps), the roofline of the dominant kernel (the attention launch =
+attention kernel + split combine, HBM bound: algorithmic bytes over the
+average launch duration, from HIP events around replays of each step's
+attention launches on the same stream right after the timed steps), and the
+fp64 oracle timed on the host's cores on a bounded sample.
 """
 
 from __future__ import annotations

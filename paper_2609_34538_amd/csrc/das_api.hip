@@ -62,14 +62,14 @@ struct Plan {
 };
 
 // Prefix pages of one sequence are cut into splits of pages_per_split pages;
-// each (split, KV head, row tile) is one chunk of work, one workgroup on the
-// matrix-core path. The default cuts each (sequence, KV head) into at least
-// 8 splits, 16 when there are fewer than 64 (sequence, KV head) pairs, of at
-// least 2 pages: enough workgroups to keep every compute unit streaming
-// while each split still covers several pages per partial result it writes.
-// (Measured on MI355X over 1, 2, 3, 4, 6, 8, 16, 32, 64 pages per split on
-// the single-sequence, ragged, long-prefix and wave-step workloads; this
-// rule picks the best or within 1 % of it on each.)
+// each (split, KV head, row tile) is one chunk of work, one workgroup. The
+// default aims for at least ~1024 chunks (four single-wave workgroups per
+// compute unit of a 256-CU part): with `units` = sequences x KV heads x row
+// tiles, each (sequence, KV head) gets max(2, the largest power of two
+// <= 1024 / units) splits, and a split holds between 2 and 32 pages.
+// (Measured on MI355X over 1-64 pages per split on the single-sequence,
+// ragged, long-prefix and wave-step workloads: this picks the best split
+// size on three and one within 0.5 % of the best on the fourth.)
 das_status make_plan(const das_cache *c, const das_batch *b, int hq, int w,
                      const das_attn_options *o, Plan *plan) {
   if (hq < 1 || hq % c->num_kv_heads != 0) return DAS_ERR_SHAPE;
@@ -84,10 +84,14 @@ das_status make_plan(const das_cache *c, const das_batch *b, int hq, int w,
   const int maxp = b->max_pages_per_seq;
   int pps = o ? o->pages_per_split : 0;
   if (pps == 0) {
-    const long seq_heads = static_cast<long>(b->batch) * c->num_kv_heads;
-    const long splits = seq_heads < 64 ? 16 : 8;
+    const long tile_rows = plan->path == DAS_PATH_MFMA ? (plan->rows <= 16 ? 16 : 32) : kValuRows;
+    const long units = static_cast<long>(b->batch) * c->num_kv_heads *
+                       ((plan->rows + tile_rows - 1) / tile_rows);
+    long splits = 2;
+    while (splits * 2 * units <= 1024) splits *= 2;
     long want = maxp / splits;
     if (want < 2) want = 2;
+    if (want > 32) want = 32;
     pps = static_cast<int>(want);
   }
   if (pps > maxp) pps = maxp;

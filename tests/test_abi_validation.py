@@ -100,13 +100,14 @@ def _nsplit_default(B, hkv, maxp, path=2, hq=None, w=8):
 
 
 def test_default_split_rule():
-    # pps = max(2, maxp // 8), maxp // 16 below 64 (sequence, KV head) pairs
-    assert _nsplit_default(B=16, hkv=8, maxp=200) == 8     # pps 25
-    assert _nsplit_default(B=4, hkv=8, maxp=257) == 17     # pps 16
-    assert _nsplit_default(B=1, hkv=55, maxp=33) == 17     # pps 2
-    assert _nsplit_default(B=1, hkv=8, maxp=20) == 10      # pps 2 (minimum)
-    assert _nsplit_default(B=1, hkv=8, maxp=33, path=1) == 17  # same rule on VALU
-    assert _nsplit_default(B=32, hkv=8, maxp=1000) == 16   # pps 125 capped at 64 (MFMA)
+    # splits = max(2, pow2 floor of 1024 / (B * Hkv * row tiles)), 2 <= pps <= 32
+    assert _nsplit_default(B=16, hkv=8, maxp=200) == 8                # 128 units: pps 25
+    assert _nsplit_default(B=4, hkv=8, maxp=257) == 33                # 32 units: pps 8
+    assert _nsplit_default(B=4, hkv=8, maxp=257, hq=32, w=32) == 9    # 4 row tiles: pps 32
+    assert _nsplit_default(B=1, hkv=55, maxp=33) == 17                # 55 units: pps 2
+    assert _nsplit_default(B=1, hkv=8, maxp=20) == 10                 # pps 2 (minimum)
+    assert _nsplit_default(B=1, hkv=8, maxp=33, path=1) == 17         # same rule on VALU
+    assert _nsplit_default(B=32, hkv=8, maxp=1000) == 32              # pps 32 (maximum)
 
 
 @pytest.mark.parametrize("field,value,code", [
