@@ -21,6 +21,9 @@ Everything here is written from the paper's statement of the method:
 * Eq. (5)  the DAS-Wave width schedule ``W_j = min(gamma, W_init + j)``.
 * Sec. 3.4  greedy acceptance: accept in order while the proposal equals the
   target argmax; at the first mismatch emit the target prediction.
+* Sec. 3.4 / App. B.3  the target prediction is the argmax of each verifier
+  conditional; the tie-breaking rule is left to the target, and the reading
+  taken here is the lowest index among the maximal entries.
 
 Readings taken where the paper is silent (each one is listed with its
 justification in the design notes of the repository):
@@ -32,7 +35,9 @@ justification in the design notes of the repository):
 * grouped-query attention: query head ``h`` reads KV head ``h // G`` with
   ``G = Hq / Hkv`` (contiguous groups);
 * depths are 1-based, ``1..R``;
-* an empty prefix (S = 0) and an empty commit (n = 0) are legal.
+* an empty prefix (S = 0) and an empty commit (n = 0) are legal;
+* argmax: ties go to the lowest index; NaN entries never win, and a row with
+  no non-NaN entry yields index 0.
 
 Pins: this module is checked by ``tests/test_oracle_pins.py`` against a
 hand-derived worked example, a library attention routine on a different
@@ -228,3 +233,34 @@ def commit_count(accepted: int, width: int) -> int:
     if not 0 <= accepted <= width or width < 1:
         raise ValueError("bad acceptance count")
     return min(accepted + 1, width)
+
+
+def argmax_lowest(row) -> int:
+    """Target prediction of one verifier conditional (Sec. 3.4: argmax over the
+    vocabulary). Ties go to the lowest index; NaN entries are ignored, and a
+    row of NaN only yields 0. Values are compared exactly (float64 holds every
+    bf16 and fp32 value)."""
+    x = _f64(row).ravel()
+    best, arg = None, 0
+    for v in range(x.shape[0]):
+        if np.isnan(x[v]):
+            continue
+        if best is None or x[v] > best:
+            best, arg = x[v], v
+    return arg
+
+
+def greedy_verify(logits, proposals: Sequence[int], tested: Optional[int] = None):
+    """Greedy verification of one block from the verifier's outputs.
+
+    ``logits`` [w, V] are the verifier's conditionals p_1..p_w of Eq. (verify
+    conditionals) over the vocabulary, ``proposals`` are y_1..y_w and the
+    first ``tested`` (default w) are checked (Sec. 3.4). Returns
+    ``(target_pred, accepted, emitted, keep)``: the argmax of every row, the
+    number of accepted proposals, the emitted tokens, and the number of
+    verifier inputs whose full-depth K/V are retained (``commit_count``)."""
+    x = _f64(logits)
+    w = x.shape[0]
+    target_pred = [argmax_lowest(x[i]) for i in range(w)]
+    accepted, emitted = greedy_accept(list(proposals), target_pred, tested)
+    return target_pred, accepted, emitted, commit_count(accepted, w)

@@ -309,6 +309,51 @@ def test_greedy_accept_rules():
     assert [orc.commit_count(a, 4) for a in range(5)] == [1, 2, 3, 4, 4]
 
 
+def test_argmax_matches_numpy_first_occurrence():
+    """numpy documents argmax / nanargmax as returning the first occurrence of
+    the maximum: an independent routine for the lowest-index tie rule."""
+    rng = np.random.default_rng(3)
+    for _ in range(50):
+        v = int(rng.integers(1, 300))
+        row = rng.integers(-4, 5, size=v).astype(np.float64)  # many ties
+        assert orc.argmax_lowest(row) == int(np.argmax(row))
+        row[rng.random(v) < 0.2] = np.nan
+        if np.isnan(row).all():
+            assert orc.argmax_lowest(row) == 0
+        else:
+            assert orc.argmax_lowest(row) == int(np.nanargmax(row))
+
+
+def test_argmax_special_values():
+    assert orc.argmax_lowest([0.0, 3.0, 1.0, 3.0]) == 1           # tie -> lowest index
+    assert orc.argmax_lowest([-0.0, 0.0, -1.0]) == 0              # signed zeros tie
+    assert orc.argmax_lowest([np.nan, -5.0, np.nan]) == 1         # NaN never wins
+    assert orc.argmax_lowest([np.nan, np.nan]) == 0               # no candidate: 0
+    assert orc.argmax_lowest([-np.inf, -np.inf]) == 0
+    assert orc.argmax_lowest([1.0, np.inf, np.inf]) == 1
+    # bf16-representable values compare exactly in float64
+    bf = torch.tensor([1.0078125, 1.0, 1.0078125], dtype=torch.bfloat16)
+    assert orc.argmax_lowest(bf.float().numpy()) == 0
+
+
+def test_greedy_verify_from_logits():
+    """The paper's illustration through the logits: y1, y2 accepted, y3 is the
+    first mismatch, yhat3 is emitted, anchor + 2 accepted inputs kept."""
+    V = 11
+    logits = np.zeros((4, V))
+    for i, t in enumerate([5, 6, 9, 1]):
+        logits[i, t] = 2.0
+    logits[2, 10] = 2.0                       # tie with 9 at row 3: lowest index wins
+    pred, acc, emitted, keep = orc.greedy_verify(logits, [5, 6, 7, 8])
+    assert pred == [5, 6, 9, 1] and acc == 2 and emitted == [5, 6, 9] and keep == 3
+    pred, acc, emitted, keep = orc.greedy_verify(logits, [5, 6, 9, 1])
+    assert acc == 4 and emitted == [5, 6, 9, 1] and keep == 4       # m = w: no bonus
+    pred, acc, emitted, keep = orc.greedy_verify(logits, [5, 6, 9, 1], tested=3)
+    assert acc == 3 and emitted == [5, 6, 9, 1] and keep == 4       # bonus yhat_4
+    pred, acc, emitted, keep = orc.greedy_verify(logits, [0, 6, 9, 1], tested=0)
+    assert acc == 0 and emitted == [5] and keep == 1                # nothing tested
+
+
 # ----------------------------------------------------------------------------
 # Mutation test: each plausible mistake in the oracle's steps fails a pin.
 # ----------------------------------------------------------------------------
