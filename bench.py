@@ -56,6 +56,17 @@ def parse():
                     help="profiling aid: time only the attention launches")
     ap.add_argument("--eager", action="store_true",
                     help="launch every call from the host instead of replaying HIP graphs")
+    ap.add_argument("--draft-policy", default="maturev",
+                    choices=["maturev", "deepkv", "deepk", "aligned"],
+                    help="read policy of the workload's draft rounds (Eq. (4))")
+    ap.add_argument("--draft", default="workload", choices=["workload", "wave"],
+                    help="draft calls: the workload's rounds, or the DAS-Wave schedule of "
+                         "Eq. (5) (gamma 32, W_init 2, J 24 rounds, Deep K/V reads)")
+    ap.add_argument("--wave-k", type=int, default=1, help="recurrent draft updates per round")
+    ap.add_argument("--verify", default="single", choices=["single", "sweep"],
+                    help="verifier: one aligned call at R per layer, or every depth 1..R")
+    ap.add_argument("--accept", action="store_true",
+                    help="greedy acceptance on the device; its commit counts feed the commit")
     return ap.parse_args()
 
 
@@ -73,39 +84,69 @@ def algorithmic_append_bytes(wl, nk, nv, num_new):
     return 2 * int(np.sum(num_new)) * (nk + nv) * wl.layers * wl.hkv * wl.dh * e
 
 
-def cpu_baseline(cd, step_calls, seconds, tokens_per_step):
-    """Time the fp64 oracle on the calls of one step (cycled until the time
-    budget is used) and scale to tokens per second of a whole step."""
+def cpu_baseline(cd, calls, seconds, tokens_per_step, max_seqs=4, max_reads=8):
+    """Time the fp64 oracle on a bounded sample of the step's attention calls
+    and scale it to a whole step: per block width, calls are cycled over at
+    most `max_reads` distinct (layer, kappa, nu) prefix reads and the first
+    `max_seqs` sequences for that width's share of the time budget; the mean
+    time per call is scaled by sum(S_b + w) of the batch over that of the
+    sample (the oracle's work is linear in it) and summed over the step."""
     import torch
     from oracle import das_oracle as orc
     from paper_2609_34538_amd import datagen as dg
 
     cores = len(os.sched_getaffinity(0))
     torch.set_num_threads(cores)
-    prepared = []
-    for (layer, kappa, nu, q, kb, vb) in step_calls:
-        for b in range(cd.wl.batch):
-            s = int(cd.prefix_lens[b])
-            prepared.append((q[b].double().cpu().numpy(),
-                             dg.gather_prefix_k(cd, b, cd.k_plane[kappa], layer, s),
-                             dg.gather_prefix_v(cd, b, cd.v_plane[nu], layer, s),
-                             kb[b].double().cpu().numpy(), vb[b].double().cpu().numpy()))
-    per_step = len(prepared)
-    done = 0
-    t0 = time.perf_counter()
-    while True:
-        args = prepared[done % per_step]
-        orc.policy_attention(*args)
-        done += 1
-        el = time.perf_counter() - t0
-        if el >= seconds and done >= per_step:
-            break
-    steps = done / per_step
-    return {"value": tokens_per_step * steps / el, "unit": "tokens/s", "cores": cores,
+    wl = cd.wl
+    seqs = list(range(min(wl.batch, max_seqs)))
+    lens = cd.prefix_lens.astype(np.float64)
+    by_w = {}
+    for c in calls:
+        by_w.setdefault(int(c[3].shape[1]), []).append(c)
+    prefix, blocks = {}, {}
+
+    def args_of(c, b):
+        layer, kappa, nu, q, kb, vb = c
+        key = (b, layer, kappa, nu)
+        if key not in prefix:
+            s_len = int(cd.prefix_lens[b])
+            prefix[key] = (dg.gather_prefix_k(cd, b, cd.k_plane[kappa], layer, s_len),
+                           dg.gather_prefix_v(cd, b, cd.v_plane[nu], layer, s_len))
+        bkey = (b, q.data_ptr(), kb.data_ptr(), vb.data_ptr())
+        if bkey not in blocks:
+            blocks[bkey] = tuple(t[b].double().cpu().numpy() for t in (q, kb, vb))
+        qb, kbb, vbb = blocks[bkey]
+        return qb, prefix[key][0], prefix[key][1], kbb, vbb
+
+    t_call, done_total = {}, 0
+    for w, cl in by_w.items():
+        reads = []
+        for c in cl:
+            if (c[0], c[1], c[2]) not in reads and len(reads) < max_reads:
+                reads.append((c[0], c[1], c[2]))
+        sample = [c for c in cl if (c[0], c[1], c[2]) in reads]
+        budget = seconds * len(cl) / len(calls)
+        done = 0
+        t0 = time.perf_counter()
+        while True:
+            c = sample[done % len(sample)]
+            for b in seqs:
+                orc.policy_attention(*args_of(c, b))
+            done += 1
+            el = time.perf_counter() - t0
+            if el >= budget and done >= len(sample):
+                break
+        scale = float(np.sum(lens + w) / np.sum(lens[seqs] + w))
+        t_call[w] = el / done * scale
+        done_total += done
+    step_s = sum(t_call[int(c[3].shape[1])] for c in calls)
+    return {"value": tokens_per_step / step_s, "unit": "tokens/s", "cores": cores,
             "kind": "oracle",
-            "sample": (f"{done} fp64 oracle per-sequence attention calls "
-                       f"({steps:.2f} steps of {per_step} calls: draft and verify, every layer) "
-                       f"in {el:.1f} s; commit not included")}
+            "sample": (f"{done_total} fp64 oracle calls (each over {len(seqs)} of {wl.batch} "
+                       f"sequences; {sum(len(v) for v in by_w.values())} attention calls per "
+                       f"step, block widths {sorted(by_w)}) in about {seconds:.0f} s, scaled by "
+                       f"prefix length to the batch and summed over the step's calls; commit "
+                       f"not included")}
 
 
 def main():
@@ -120,31 +161,77 @@ def main():
 
     dev = "cuda"
     wl = dg.WORKLOADS[args.config]
-    rounds = list(zip(wl.draft_depths, wl.draft_widths))
-    R = wl.depth_R
-    # bytes one step reads, to size the cache rotation
+    R, L, wv = wl.depth_R, wl.layers, wl.verify_width
+    if args.draft == "wave":
+        # the verifier consumes the anchor and the schedule's final proposals
+        wv = min(32, 2 + 24)
+    # The calls of one step: (kind, layer, kappa, nu, width, block depth,
+    # rotation group). Calls of rotation group g on the step's cache copy c read copy
+    # (c + g) mod copies, so repeated reads of the same prefix bytes inside a
+    # step are also >= rotate_bytes apart.
+    plan = []
+    if args.draft == "wave":
+        J, gamma, w_init = 24, 32, 2
+        widths = [min(gamma, w_init + j) for j in range(J)]  # Eq. (5)
+        for j, w in enumerate(widths):
+            for _ in range(args.wave_k):
+                for layer in range(L):
+                    plan.append(("draft", layer, R, R, w, R, j))
+        n_groups = J
+    else:
+        pol = {"maturev": lambda d: (d, R), "deepkv": lambda d: (R, R),
+               "deepk": lambda d: (R, d), "aligned": lambda d: (d, d)}[args.draft_policy]
+        for layer in range(L):
+            for d, w in zip(wl.draft_depths, wl.draft_widths):
+                kappa, nu = pol(d)
+                plan.append(("draft", layer, kappa, nu, w, d, 0))
+        n_groups = 1
+    vdepths = [R] if args.verify == "single" else list(range(1, R + 1))
+    for r in vdepths:
+        for layer in range(L):
+            plan.append(("verify", layer, r, r, wv, r, 0))
+    kd, vd = set(wl.k_depths()), set(wl.v_depths())
+    missing = sorted({e[2] for e in plan} - kd) + sorted({e[3] for e in plan} - vd)
+    if missing:
+        print(json.dumps({"error": f"depths {missing} are not stored in workload {wl.name}"}))
+        sys.exit(2)
+
+    # bytes one step reads (and bytes between reuses of one rotation group), to
+    # size the cache rotation
     rng_lens = np.random.default_rng(wl.seed).integers(wl.prefix[0], wl.prefix[1] + 1,
                                                        size=wl.batch)
-    step_read = sum(algorithmic_attn_bytes(wl, rng_lens, w) for _, w in rounds) * wl.layers
-    step_read += algorithmic_attn_bytes(wl, rng_lens, wl.verify_width) * wl.layers
-    copies = max(1, min(16, math.ceil(args.rotate_bytes / max(step_read, 1))))
-    cd = dg.make_cache(wl, dev, copies=copies)
+    step_read = sum(algorithmic_attn_bytes(wl, rng_lens, e[4]) for e in plan)
+    if n_groups > 1:
+        group_read = step_read / n_groups
+        copies = 1 + math.ceil(args.rotate_bytes / max(group_read, 1))
+    else:
+        copies = math.ceil(args.rotate_bytes / max(step_read, 1))
+    copies = max(1, min(16, copies))
+    cd = dg.make_cache(wl, dev, copies=copies, spare_tokens=max(wl.w_max, wv))
     lens = cd.prefix_lens
     cache = das.PagedCache(cd.k_pool, cd.v_pool, R, cd.k_plane, cd.v_plane)
     batches = [das.Batch(torch.as_tensor(lens.astype(np.int32), device=dev),
                          torch.as_tensor(t, device=dev)) for t in cd.tables]
-    # per-round block inputs; the verifier's block K/V is the commit source
-    draft_in = [dg.block_inputs(cd, w, d, dev) for d, w in rounds]
-    qv, _, _ = dg.block_inputs(cd, wl.verify_width, R, dev)
-    k_new, v_new, num_new = dg.commit_inputs(cd, wl.verify_width, dev)
+    # Block inputs per (width, depth); the verifier's block K/V at every stored
+    # plane are the commit source.
+    k_new, v_new, num_new = dg.commit_inputs(cd, wv, dev)
     num_new_t = torch.as_tensor(num_new, device=dev)
-    kp, vp = cd.k_plane[R], cd.v_plane[R]
+    block_in, outs = {}, {}
+    for _, layer, kappa, nu, w, depth, _ in plan:
+        if (w, depth) not in block_in:
+            block_in[(w, depth)] = dg.block_inputs(cd, w, depth, dev)
+            outs[(w, depth)] = torch.empty_like(block_in[(w, depth)][0])
     opts = dict(path=args.path, pages_per_split=args.pps)
-    wmax = max(w for _, w in rounds + [(R, wl.verify_width)])
+    wmax = max(e[4] for e in plan)
     ws = das.alloc_workspace(cache, batches[0], wl.hq, wmax, **opts)
-    outs = [torch.empty_like(q) for q, _, _ in draft_in]
-    out_v = torch.empty_like(qv)
     len_out = torch.empty(wl.batch, dtype=torch.int32, device=dev)
+    if args.accept:
+        y_t, yhat_t, m_t = dg.accept_inputs(wl.batch, wv, wl.seed, device=dev)
+        acc_t = torch.empty(wl.batch, dtype=torch.int32, device=dev)
+        keep_t = torch.empty(wl.batch, dtype=torch.int32, device=dev)
+        commit_count_t = keep_t
+    else:
+        commit_count_t = num_new_t
     # A stream of its own (default priority): graphs cannot be captured on
     # the legacy default stream.
     # Graph replays launch on the current stream, so it is made current.
@@ -152,24 +239,27 @@ def main():
     torch.cuda.synchronize()
     torch.cuda.set_stream(stream)
 
-    # Every call of a step, marshalled once per cache copy: the Mature-V
-    # draft of each layer (and round), the verifier of each layer, the commit.
+    def attn_args(kind, layer, w, depth):
+        q, kb, vb = block_in[(w, depth)]
+        if kind == "verify":
+            # the verifier's block K/V are the committed entries of plane `depth`
+            kb, vb = k_new[cd.k_plane[depth], layer], v_new[cd.v_plane[depth], layer]
+        return q, kb, vb, outs[(w, depth)]
+
+    # Every call of a step, marshalled once per starting cache copy.
     step_calls = []
-    for batch in batches:
+    for c in range(copies):
         seq = []
-        for layer in range(wl.layers):
-            for r, (d, w) in enumerate(rounds):
-                q, kb, vb = draft_in[r]
-                seq.append((w, das.PreparedAttention(cache, batch, layer, d, R, q, kb, vb, outs[r],
-                                                     ws, stream=stream, **opts)))
-        for layer in range(wl.layers):
-            seq.append((wl.verify_width,
-                        das.PreparedAttention(cache, batch, layer, R, R, qv, k_new[kp, layer],
-                                              v_new[vp, layer], out_v, ws, stream=stream,
-                                              **opts)))
+        for kind, layer, kappa, nu, w, depth, g in plan:
+            q, kb, vb, out = attn_args(kind, layer, w, depth)
+            seq.append((w, das.PreparedAttention(cache, batches[(c + g) % copies], layer, kappa,
+                                                 nu, q, kb, vb, out, ws, stream=stream, **opts)))
+        if args.accept:
+            seq.append((None, lambda: das.greedy_accept(y_t, yhat_t, m_t, accepted=acc_t,
+                                                        num_keep=keep_t, stream=stream)))
         if not args.attn_only:
-            seq.append((None, das.PreparedAppend(cache, batch, k_new, v_new, num_new_t, len_out,
-                                                 stream=stream)))
+            seq.append((None, das.PreparedAppend(cache, batches[c], k_new, v_new, commit_count_t,
+                                                 len_out, stream=stream)))
         step_calls.append(seq)
     n_attn = sum(1 for w, _ in step_calls[0] if w is not None)
     widths = [w for w, _ in step_calls[0] if w is not None]
@@ -232,7 +322,7 @@ def main():
     torch.cuda.synchronize()
     total_ms = t_start.elapsed_time(t_end)
     ms_step = total_ms / args.steps
-    tokens_per_step = wl.batch * wl.verify_width  # block tokens verified per step
+    tokens_per_step = wl.batch * wv  # block tokens verified per step
     value = tokens_per_step / (ms_step / 1e3)
 
     if not args.eager:
@@ -253,8 +343,7 @@ def main():
     attn_ms = attn_total_ms / len(launches)
     bytes_per = float(np.mean([algorithmic_attn_bytes(wl, lens, w) for w in launches]))
     achieved = bytes_per / (attn_ms / 1e3) / 1e9
-    step_bytes = (sum(algorithmic_attn_bytes(wl, lens, w) for _, w in rounds) * wl.layers
-                  + algorithmic_attn_bytes(wl, lens, wl.verify_width) * wl.layers
+    step_bytes = (sum(algorithmic_attn_bytes(wl, lens, e[4]) for e in plan)
                   + (0 if args.attn_only else
                      algorithmic_append_bytes(wl, cd.k_pool.shape[0], cd.v_pool.shape[0],
                                               num_new)))
@@ -275,8 +364,11 @@ def main():
         "config": {"workload": wl.name, "batch": wl.batch, "q_heads": wl.hq,
                    "kv_heads": wl.hkv, "head_dim": wl.dh, "prefix_len": [int(lens.min()),
                                                                           int(lens.max())],
-                   "draft_blocks": [{"depth": d, "width": w} for d, w in rounds],
-                   "verify": {"depth": R, "width": wl.verify_width}, "depth_R": R,
+                   "draft": (f"das-wave J=24 gamma=32 W_init=2 k={args.wave_k}"
+                             if args.draft == "wave" else "workload rounds"),
+                   "draft_calls": sorted({(e[2], e[3], e[4]) for e in plan if e[0] == "draft"}),
+                   "verify": {"depths": [vdepths[0], vdepths[-1]], "width": wv},
+                   "depth_R": R, "accept_on_device": args.accept,
                    "core_layers": wl.layers, "path": args.path,
                    "pages_per_split": args.pps, "cache_copies_rotated": copies,
                    "launch": "eager" if args.eager else "hip_graph",
@@ -294,11 +386,9 @@ def main():
     }
     if not args.no_cpu:
         calls = []
-        for layer in range(wl.layers):
-            for r, (d, w) in enumerate(rounds):
-                q, kb, vb = draft_in[r]
-                calls.append((layer, d, R, q, kb, vb))
-            calls.append((layer, R, R, qv, k_new[kp, layer], v_new[vp, layer]))
+        for kind, layer, kappa, nu, w, depth, _ in plan:
+            q, kb, vb, _ = attn_args(kind, layer, w, depth)
+            calls.append((layer, kappa, nu, q, kb, vb))
         result["cpu_baseline"] = cpu_baseline(cd, calls, args.cpu_seconds, tokens_per_step)
     print(json.dumps(result))
 

@@ -83,6 +83,7 @@ typedef enum das_dtype { DAS_F32 = 0, DAS_BF16 = 1 } das_dtype;
 #define DAS_DEVERR_PREFIX 2u     /* prefix_len[b] < 0 or beyond the table's pages */
 #define DAS_DEVERR_COMMIT 4u     /* num_new[b] outside [0, w_max], or the commit
                                     would run past the sequence's table pages     */
+#define DAS_DEVERR_TESTED 8u     /* tested[b] outside [0, block_len]; clamped      */
 
 /*
  * Depth-indexed, paged KV cache (caller-owned device memory).
@@ -243,6 +244,41 @@ das_status das_kv_append(const das_cache *cache, const das_batch *batch,
                          const void *k_new, const void *v_new, int32_t w_max,
                          const int32_t *num_new, int32_t *len_out,
                          hipStream_t stream);
+
+/*
+ * Greedy verification of a block on the device (Sec. 3.4), so that the
+ * commit count reaches das_kv_append without a host round trip.
+ *
+ * For each sequence b, the first m_b = tested[b] proposals are checked in
+ * order against the verifier's predictions; proposals are accepted while
+ * y_i equals yhat_i (i = 1..m_b). With a_b accepted:
+ *   - emitted tokens: y_1..y_{a_b}, then yhat_{a_b+1} when a_b < w (the
+ *     target prediction at the first mismatch, or the bonus token from an
+ *     unused conditional when all m_b < w tested proposals agree); w tokens
+ *     when every proposal of a full block is accepted;
+ *   - retained verifier inputs: num_keep[b] = min(a_b + 1, w) (the anchor and
+ *     the accepted inputs among [x_t, y_1 .. y_{w-1}]).
+ *
+ *   proposals   device [B][w] int32: y_1..y_w (index i-1 holds y_i)
+ *   target_pred device [B][w] int32: yhat_i = argmax of the verifier's
+ *               conditional p_i (computed by the model's readout)
+ *   tested      device [B] int32 m_b in 0..w, or NULL for m_b = w; values
+ *               outside 0..w are clamped and reported with DAS_DEVERR_TESTED
+ *   accepted    device [B] int32, written: a_b
+ *   num_keep    device [B] int32, written: min(a_b + 1, w); pass it as the
+ *               num_new argument of das_kv_append (w_max = w)
+ *   emitted     device [B][w] int32 or NULL, written: the emitted tokens;
+ *               entries past num_emitted[b] are left untouched
+ *   num_emitted device [B] int32 or NULL, written: min(a_b + 1, w)
+ *   dev_error   optional device word (DAS_DEVERR_TESTED)
+ *
+ * batch >= 1; block_len w in 1..DAS_MAX_BLOCK. Integer work only: results
+ * are exact. The output arrays must not overlap the inputs.
+ */
+das_status das_greedy_accept(int32_t batch, int32_t block_len, const int32_t *proposals,
+                             const int32_t *target_pred, const int32_t *tested,
+                             int32_t *accepted, int32_t *num_keep, int32_t *emitted,
+                             int32_t *num_emitted, uint32_t *dev_error, hipStream_t stream);
 
 /* Static description of a status code; never NULL. */
 const char *das_status_string(das_status status);

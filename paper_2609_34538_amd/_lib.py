@@ -31,11 +31,11 @@ STATUS_NAMES = {0: "DAS_OK", -1: "DAS_ERR_NULL", -2: "DAS_ERR_SHAPE", -3: "DAS_E
                 -7: "DAS_ERR_UNSUPPORTED", -8: "DAS_ERR_ALIGN"}
 DTYPE_CODES = {torch.float32: 0, torch.bfloat16: 1}
 PATHS = {"auto": 0, "valu": 1, "mfma": 2}
-DEVERR_PAGE, DEVERR_PREFIX, DEVERR_COMMIT = 1, 2, 4
+DEVERR_PAGE, DEVERR_PREFIX, DEVERR_COMMIT, DEVERR_TESTED = 1, 2, 4, 8
 
 EXPORTED = ["das_attn_workspace_bytes", "das_attn_workspace_bytes_ex", "das_attn_draft_maturev",
-            "das_attn_verify", "das_attn_policy", "das_kv_append", "das_status_string",
-            "das_version"]
+            "das_attn_verify", "das_attn_policy", "das_kv_append", "das_greedy_accept",
+            "das_status_string", "das_version"]
 
 
 class DasError(RuntimeError):
@@ -83,6 +83,8 @@ def _load() -> ctypes.CDLL:
     lib.das_kv_append.argtypes = [pc, pb, c_void_p, c_void_p, c_int32, c_void_p, c_void_p,
                                   c_void_p]
     lib.das_kv_append.restype = c_int32
+    lib.das_greedy_accept.argtypes = [c_int32, c_int32] + [c_void_p] * 8 + [c_void_p]
+    lib.das_greedy_accept.restype = c_int32
     lib.das_status_string.argtypes = [c_int32]
     lib.das_status_string.restype = c_char_p
     lib.das_version.argtypes = []
@@ -362,3 +364,33 @@ def kv_append(cache: PagedCache, batch: Batch, k_new: torch.Tensor, v_new: torch
                            _stream_handle(stream))
     if st != DAS_OK:
         raise DasError(st, "das_kv_append")
+
+
+def _i32(t: Optional[torch.Tensor], shape, what: str):
+    if t is None:
+        return None
+    if t.dtype != torch.int32 or tuple(t.shape) != tuple(shape) or not t.is_contiguous():
+        raise ValueError(f"{what} must be a contiguous int32 tensor of shape {tuple(shape)}")
+    return t.data_ptr()
+
+
+def greedy_accept(proposals: torch.Tensor, target_pred: torch.Tensor,
+                  tested: Optional[torch.Tensor] = None, accepted: Optional[torch.Tensor] = None,
+                  num_keep: Optional[torch.Tensor] = None, emitted: Optional[torch.Tensor] = None,
+                  num_emitted: Optional[torch.Tensor] = None,
+                  dev_error: Optional[torch.Tensor] = None, stream=None):
+    """Greedy verification of a block on the device (Sec. 3.4). Returns
+    (accepted, num_keep); num_keep is das_kv_append's num_new."""
+    B, w = proposals.shape
+    if accepted is None:
+        accepted = torch.empty(B, dtype=torch.int32, device=proposals.device)
+    if num_keep is None:
+        num_keep = torch.empty(B, dtype=torch.int32, device=proposals.device)
+    args = (_i32(proposals, (B, w), "proposals"), _i32(target_pred, (B, w), "target_pred"),
+            _i32(tested, (B,), "tested"), _i32(accepted, (B,), "accepted"),
+            _i32(num_keep, (B,), "num_keep"), _i32(emitted, (B, w), "emitted"),
+            _i32(num_emitted, (B,), "num_emitted"), _ptr(dev_error))
+    st = LIB.das_greedy_accept(B, w, *args, _stream_handle(stream))
+    if st != DAS_OK:
+        raise DasError(st, "das_greedy_accept")
+    return accepted, num_keep

@@ -261,6 +261,31 @@ das_status das_kv_append(const das_cache *cache, const das_batch *batch, const v
   return DAS_OK;
 }
 
+das_status das_greedy_accept(int32_t batch, int32_t block_len, const int32_t *proposals,
+                             const int32_t *target_pred, const int32_t *tested,
+                             int32_t *accepted, int32_t *num_keep, int32_t *emitted,
+                             int32_t *num_emitted, uint32_t *dev_error, hipStream_t stream) {
+  if (!proposals || !target_pred || !accepted || !num_keep) return DAS_ERR_NULL;
+  if (batch < 1 || block_len < 1 || block_len > DAS_MAX_BLOCK) return DAS_ERR_SHAPE;
+  if (!aligned(proposals, 4) || !aligned(target_pred, 4) || !aligned(tested, 4) ||
+      !aligned(accepted, 4) || !aligned(num_keep, 4) || !aligned(emitted, 4) ||
+      !aligned(num_emitted, 4) || !aligned(dev_error, 4))
+    return DAS_ERR_ALIGN;
+  AcceptParams p;
+  p.proposals = proposals;
+  p.target_pred = target_pred;
+  p.tested = tested;
+  p.accepted = accepted;
+  p.num_keep = num_keep;
+  p.emitted = emitted;
+  p.num_emitted = num_emitted;
+  p.dev_error = dev_error;
+  p.batch = batch;
+  p.w = block_len;
+  if (launch_greedy_accept(p, stream) != hipSuccess) return DAS_ERR_HIP;
+  return DAS_OK;
+}
+
 const char *das_status_string(das_status status) {
   switch (status) {
     case DAS_OK: return "ok";

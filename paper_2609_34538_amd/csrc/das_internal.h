@@ -57,6 +57,16 @@ hipError_t launch_attn_combine(const AttnParams &p, int dtype, int dh, int skip_
                                hipStream_t s);
 hipError_t launch_kv_append(const AppendParams &p, int dtype, int dh, hipStream_t s);
 
+struct AcceptParams {
+  const int32_t *proposals;    // [B][w]
+  const int32_t *target_pred;  // [B][w]
+  const int32_t *tested;       // [B] or null (= w)
+  int32_t *accepted, *num_keep, *emitted, *num_emitted;  // emitted / num_emitted may be null
+  uint32_t *dev_error;
+  int32_t batch, w;
+};
+hipError_t launch_greedy_accept(const AcceptParams &p, hipStream_t s);
+
 // Query rows of one workgroup of the vector-ALU kernel.
 constexpr int kValuRows = 32;
 

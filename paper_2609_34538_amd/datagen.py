@@ -245,3 +245,22 @@ def gather_prefix_v(cd: CacheData, b: int, plane: int, layer: int, s_len: int,
     t = cd.v_pool[plane, layer].index_select(1, pages)         # [Hkv, npg, 8, dh, 8]
     t = t.permute(1, 2, 4, 0, 3).reshape(npg * PAGE, cd.wl.hkv, cd.wl.dh)[:s_len]
     return t.double().cpu().numpy()
+
+
+def accept_inputs(batch: int, width: int, seed: int, vocab: int = 65536, device="cuda",
+                  random_tested: bool = False):
+    """Seeded verifier predictions yhat [B, w], proposals y [B, w] and tested
+    counts m [B] (int32). Each sequence's proposals agree with the predictions
+    on a leading run of U{0..w} positions and differ at the next one, so every
+    acceptance length occurs; m = w unless random_tested (then U{0..w})."""
+    rng = np.random.default_rng(seed)
+    yhat = rng.integers(0, vocab, size=(batch, width))
+    y = rng.integers(0, vocab, size=(batch, width))
+    run = rng.integers(0, width + 1, size=batch)
+    for b in range(batch):
+        y[b, :run[b]] = yhat[b, :run[b]]
+        if run[b] < width:
+            y[b, run[b]] = (yhat[b, run[b]] + 1 + rng.integers(0, vocab - 1)) % vocab
+    m = rng.integers(0, width + 1, size=batch) if random_tested else np.full(batch, width)
+    t = lambda x: torch.as_tensor(np.ascontiguousarray(x).astype(np.int32), device=device)
+    return t(y), t(yhat), t(m)

@@ -27,6 +27,6 @@ def test_exports_every_declared_function():
 
 
 def test_status_strings_and_version():
-    for code in (0, -1, -2, -3, -4, -5, -6, -7, 12345):
+    for code in (0, -1, -2, -3, -4, -5, -6, -7, -8, 12345):
         assert LIB.das_status_string(code)
     assert LIB.das_version() >= 100

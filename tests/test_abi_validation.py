@@ -204,3 +204,19 @@ def test_append_argument_checks():
     nb = make_batch()
     nb.block_table = None
     assert app(bb=nb) == NULL
+
+
+def test_greedy_accept_argument_checks():
+    def acc(B=4, w=8, y=FAKE, yhat=FAKE, m=None, a=FAKE, keep=FAKE, em=None, nem=None, err=None):
+        return LIB.das_greedy_accept(B, w, y, yhat, m, a, keep, em, nem, err, None)
+    assert acc(y=None) == NULL
+    assert acc(yhat=None) == NULL
+    assert acc(a=None) == NULL
+    assert acc(keep=None) == NULL
+    assert acc(B=0) == SHAPE
+    assert acc(w=0) == SHAPE
+    assert acc(w=65) == SHAPE
+    assert acc(y=FAKE + 2) == ALIGN
+    assert acc(m=FAKE + 1) == ALIGN
+    assert acc(em=FAKE + 2) == ALIGN
+    assert acc(err=FAKE + 3) == ALIGN
