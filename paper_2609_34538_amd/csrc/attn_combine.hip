@@ -13,33 +13,45 @@ namespace das {
 namespace {
 
 constexpr int kRowsPerBlock = 8;
+constexpr int kColsPerBlock = 32;
 constexpr int kEager = 16;  // splits whose partials are loaded before the count is known
 
-// One workgroup per (sequence, KV head, group of 8 rows); one thread per
-// (row, 4 consecutive columns). The partials of the first 16 splits that the
-// workspace can hold are loaded together with the prefix length, so a merge
-// of up to 16 splits costs one memory round trip; values of splits past the
-// sequence's count are discarded by selection, never used in arithmetic.
+// One single-wave workgroup per (sequence, KV head, 8 rows, 32 columns); one
+// thread per (row, 4 consecutive columns). A row's per-split maxima and sums
+// are contiguous, so they arrive as 16-byte vectors; the partials of the first
+// 16 splits the workspace holds are loaded together with the prefix length,
+// so a merge of up to 16 splits costs one memory round trip. Values of splits
+// past the sequence's count are discarded by selection, never used in
+// arithmetic.
 template <typename T, int DH>
-__global__ __launch_bounds__(kRowsPerBlock * DH / 4) void attn_combine_kernel(AttnParams p,
-                                                                              int skip_single) {
+__global__ __launch_bounds__(64) void attn_combine_kernel(AttnParams p, int skip_single) {
   const int unit = blockIdx.x;  // b * hkv + kvh
   const int b = unit / p.hkv;
   const int kvh = unit % p.hkv;
-  const int row = blockIdx.y * kRowsPerBlock + threadIdx.x / (DH / 4);
-  const int c = 4 * (threadIdx.x % (DH / 4));
-  const bool live = row < p.rows;
-  const size_t base_row = (static_cast<size_t>(unit) * p.nsplit) * p.rows + (live ? row : 0);
+  const int row = blockIdx.y * kRowsPerBlock + threadIdx.x / 8;
+  const int c = blockIdx.z * kColsPerBlock + 4 * (threadIdx.x % 8);
+  const bool live = row < p.rows && c < DH;
+  const int r0 = live ? row : 0, c0 = live ? c : 0;
+  const size_t obase = (static_cast<size_t>(unit) * p.nsplit) * p.rows + r0;  // split 0's row
+  const size_t mbase = (static_cast<size_t>(unit) * p.rows + r0) * p.nsplit_ml;
 
   const int s_raw = p.prefix_len[b];
   float mv[kEager], lv[kEager];
   float4 ov[kEager];
 #pragma unroll
+  for (int k4 = 0; k4 < kEager / 4; ++k4) {
+    const bool have = 4 * k4 < p.nsplit_ml;  // uniform
+    const float4 m4 = have ? *reinterpret_cast<const float4 *>(p.ws_m + mbase + 4 * k4)
+                           : make_float4(0.f, 0.f, 0.f, 0.f);
+    const float4 l4 = have ? *reinterpret_cast<const float4 *>(p.ws_l + mbase + 4 * k4)
+                           : make_float4(0.f, 0.f, 0.f, 0.f);
+    mv[4 * k4] = m4.x, mv[4 * k4 + 1] = m4.y, mv[4 * k4 + 2] = m4.z, mv[4 * k4 + 3] = m4.w;
+    lv[4 * k4] = l4.x, lv[4 * k4 + 1] = l4.y, lv[4 * k4 + 2] = l4.z, lv[4 * k4 + 3] = l4.w;
+  }
+#pragma unroll
   for (int k = 0; k < kEager; ++k) {
-    const size_t r = base_row + static_cast<size_t>(k < p.nsplit ? k : 0) * p.rows;
-    mv[k] = p.ws_m[r];
-    lv[k] = p.ws_l[r];
-    ov[k] = *reinterpret_cast<const float4 *>(p.ws_o + r * DH + c);
+    const size_t r = obase + static_cast<size_t>(k < p.nsplit ? k : 0) * p.rows;
+    ov[k] = *reinterpret_cast<const float4 *>(p.ws_o + r * DH + c0);
   }
   bool bad;
   const int S = clamp_prefix(s_raw, p.max_pages, &bad);
@@ -65,9 +77,8 @@ __global__ __launch_bounds__(kRowsPerBlock * DH / 4) void attn_combine_kernel(At
   }
   // splits beyond the first 16, merged in the same online form
   for (int s0 = kEager; s0 < ns; ++s0) {
-    const size_t r = base_row + static_cast<size_t>(s0) * p.rows;
-    const float m = p.ws_m[r], l = p.ws_l[r];
-    const float4 o = *reinterpret_cast<const float4 *>(p.ws_o + r * DH + c);
+    const float m = p.ws_m[mbase + s0], l = p.ws_l[mbase + s0];
+    const float4 o = *reinterpret_cast<const float4 *>(p.ws_o + (obase + static_cast<size_t>(s0) * p.rows) * DH + c);
     const float nm = fmaxf(mx, m);
     const float a = exp2f(mx - nm), sc = exp2f(m - nm);
     den = den * a + sc * l;
@@ -91,9 +102,9 @@ __global__ __launch_bounds__(kRowsPerBlock * DH / 4) void attn_combine_kernel(At
 
 template <typename T, int DH>
 hipError_t launch_typed(const AttnParams &p, int skip_single, hipStream_t s) {
-  dim3 grid(p.batch * p.hkv, (p.rows + kRowsPerBlock - 1) / kRowsPerBlock);
-  hipLaunchKernelGGL((attn_combine_kernel<T, DH>), grid, dim3(kRowsPerBlock * DH / 4), 0, s, p,
-                     skip_single);
+  dim3 grid(p.batch * p.hkv, (p.rows + kRowsPerBlock - 1) / kRowsPerBlock,
+            (DH + kColsPerBlock - 1) / kColsPerBlock);
+  hipLaunchKernelGGL((attn_combine_kernel<T, DH>), grid, dim3(64), 0, s, p, skip_single);
   return hipGetLastError();
 }
 

@@ -396,8 +396,10 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, i
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) *reinterpret_cast<f32x4 *>(orow + 16 * dt + 4 * lg) = st.o[qt][dt];
       if (lg == 0) {
-        p.ws_m[prow0 + row] = st.m[qt] == kNegInf ? 0.f : st.m[qt];
-        p.ws_l[prow0 + row] = st.l[qt];
+        const size_t mrow =
+            ((static_cast<size_t>(b) * p.hkv + kvh) * p.rows + row) * p.nsplit_ml + split;
+        p.ws_m[mrow] = st.m[qt] == kNegInf ? 0.f : st.m[qt];
+        p.ws_l[mrow] = st.l[qt];
       }
     }
   }

@@ -180,8 +180,10 @@ __global__ __launch_bounds__(256) void attn_valu_kernel(AttnParams p) {
       if (col < DH) p.ws_o[prow * DH + col] = acc[k][c];
     }
     if (lane == 0) {
-      p.ws_m[prow] = m[k];
-      p.ws_l[prow] = l[k];
+      const size_t mrow =
+          ((static_cast<size_t>(b) * p.hkv + kvh) * p.rows + row) * p.nsplit_ml + split;
+      p.ws_m[mrow] = m[k];
+      p.ws_l[mrow] = l[k];
     }
   }
 }

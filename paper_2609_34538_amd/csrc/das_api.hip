@@ -58,6 +58,7 @@ struct Plan {
   int rows;             // w * G query rows per (sequence, kv head)
   int pages_per_split;
   int nsplit;
+  int nsplit_ml;        // nsplit rounded up to a multiple of 4
   size_t ws_o_bytes, ws_ml_bytes, total;
 };
 
@@ -100,8 +101,10 @@ das_status make_plan(const das_cache *c, const das_batch *b, int hq, int w,
   plan->nsplit = (maxp + pps - 1) / pps;
   const size_t per_split_rows =
       static_cast<size_t>(b->batch) * c->num_kv_heads * plan->nsplit * plan->rows;
+  plan->nsplit_ml = (plan->nsplit + 3) & ~3;
   plan->ws_o_bytes = align_up(per_split_rows * c->head_dim * sizeof(float));
-  plan->ws_ml_bytes = align_up(per_split_rows * sizeof(float));
+  plan->ws_ml_bytes = align_up(static_cast<size_t>(b->batch) * c->num_kv_heads * plan->rows *
+                               plan->nsplit_ml * sizeof(float));
   plan->total = plan->ws_o_bytes + 2 * plan->ws_ml_bytes;
   return DAS_OK;
 }
@@ -159,6 +162,7 @@ das_status attn_common(const das_cache *c, const das_batch *b, int layer, int ka
   p.max_pages = b->max_pages_per_seq;
   p.pages_per_split = plan.pages_per_split;
   p.nsplit = plan.nsplit;
+  p.nsplit_ml = plan.nsplit_ml;
   // log2(e) / sqrt(dh): logits are kept in base-2 units so exp2 can be used.
   const double log2e = 1.4426950408889634074;
   p.scale_log2 = static_cast<float>(log2e / __builtin_sqrt(static_cast<double>(dh)));

@@ -26,12 +26,13 @@ struct AttnParams {
   const int32_t *prefix_len;   // [B]
   const int32_t *block_table;  // [B][max_pages]
   uint32_t *dev_error;         // or nullptr
-  float *ws_o;           // [B][Hkv][nsplit][rows][dh]   unnormalised partial O
-  float *ws_m;           // [B][Hkv][nsplit][rows]       running max (log2 units)
-  float *ws_l;           // [B][Hkv][nsplit][rows]       running sum
+  float *ws_o;           // [B][Hkv][nsplit][rows][dh]     unnormalised partial O
+  float *ws_m;           // [B][Hkv][rows][nsplit_ml]      running max (log2 units)
+  float *ws_l;           // [B][Hkv][rows][nsplit_ml]      running sum
   int32_t batch, hq, hkv, group, w, rows;  // rows = w * group
   int32_t num_pages, max_pages;
   int32_t pages_per_split, nsplit;
+  int32_t nsplit_ml;     // nsplit rounded up to a multiple of 4 (16-byte rows of m, l)
   float scale_log2;      // log2(e) / sqrt(dh): logits in base-2 units
 };
 

@@ -82,7 +82,8 @@ def test_workspace_size_formula():
     rows, hkv, B, maxp, dh = 8 * 4, 8, 4, 10, 128
     per = B * hkv * maxp * rows
     al = lambda x: (x + 255) // 256 * 256
-    assert ws_bytes(c, b, opts=o) == al(per * dh * 4) + 2 * al(per * 4)
+    # partial O per split and row; m and l per row with the splits padded to 4
+    assert ws_bytes(c, b, opts=o) == al(per * dh * 4) + 2 * al(B * hkv * rows * 12 * 4)
 
 
 def _nsplit_default(B, hkv, maxp, path=2, hq=None, w=8):
@@ -94,7 +95,7 @@ def _nsplit_default(B, hkv, maxp, path=2, hq=None, w=8):
     n = ws_bytes(c, b, hq=hq, w=w, opts=o)
     for ns in range(1, maxp + 1):
         al = lambda x: (x + 255) // 256 * 256
-        if al(per_split * ns * 128 * 4) + 2 * al(per_split * ns * 4) == n:
+        if al(per_split * ns * 128 * 4) + 2 * al(per_split * ((ns + 3) // 4 * 4) * 4) == n:
             return ns
     raise AssertionError("no split count matches the workspace size")
 
