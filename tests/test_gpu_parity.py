@@ -28,6 +28,9 @@ def small_workloads():
         "c5s": dg.scaled(W[5], batch=4, hq=3, hkv=3, layers=2, prefix=(100, 400)),
         "gqa8_dh64": dg.scaled(W[4], batch=2, hq=16, hkv=2, dh=64, layers=1, prefix=(130, 190),
                                draft_widths=(5,), verify_width=5, paged_random=True),
+        # 32 x 8 = 256 query rows: two workgroups of 4 row tiles per split
+        "gqa8_w32": dg.scaled(W[4], batch=2, hq=16, hkv=2, dh=128, layers=1, prefix=(100, 200),
+                              draft_widths=(32,), verify_width=32, paged_random=True),
     }
 
 
