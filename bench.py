@@ -39,6 +39,25 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0
 
+# HBM bytes per attention launch (kernel + split merge) from rocprofv3
+# FETCH_SIZE / WRITE_SIZE passes over this benchmark's default command, each
+# scaled by what the counter reads for a plain 1 GiB copy; valid only for the
+# kernel sources with this digest, the default workload and library plan.
+MEASURED_TRAFFIC = {("single-seq-looped-bf16", "df323653c50bcdba"): 50_603_603}
+TRAFFIC_SOURCES = ["paper_2609_34538_amd/csrc/attn_mfma.hip",
+                   "paper_2609_34538_amd/csrc/attn_combine.hip",
+                   "paper_2609_34538_amd/csrc/das_api.hip",
+                   "paper_2609_34538_amd/csrc/das_internal.h"]
+
+
+def kernel_digest():
+    import hashlib
+    h = hashlib.sha256()
+    for f in TRAFFIC_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
 
 def parse():
     ap = argparse.ArgumentParser()
@@ -67,6 +86,8 @@ def parse():
                     help="verifier: one aligned call at R per layer, or every depth 1..R")
     ap.add_argument("--accept", action="store_true",
                     help="greedy acceptance on the device; its commit counts feed the commit")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only copy 1 GiB device to device once (reference for HBM counters)")
     return ap.parse_args()
 
 
@@ -156,6 +177,15 @@ def main():
                           "n_gpus": args.gpus}))
         sys.exit(2)
     import torch
+    if args.copy_calibration:
+        n = 1 << 30
+        src = torch.ones(n // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes": n}))
+        return
     from paper_2609_34538_amd import _lib as das
     from paper_2609_34538_amd import datagen as dg
 
@@ -348,6 +378,9 @@ def main():
                      algorithmic_append_bytes(wl, cd.k_pool.shape[0], cd.v_pool.shape[0],
                                               num_new)))
 
+    default_plan = (args.path == "auto" and args.pps == 0 and args.draft == "workload"
+                    and args.draft_policy == "maturev" and args.verify == "single")
+    traffic = MEASURED_TRAFFIC.get((wl.name, kernel_digest())) if default_plan else None
     result = {
         "metric": "Mature-V draft-block attention tokens/s + achieved HBM GB/s (% of 8 TB/s)",
         "value": value,
@@ -376,7 +409,7 @@ def main():
         "step_hbm_gbs": step_bytes / (ms_step / 1e3) / 1e9,
         "step_frac_of_8tbs": step_bytes / (ms_step / 1e3) / 1e9 / HBM_PEAK_GBS,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "kernel": "attention launch (partial + split combine)",
                      "timing": ("HIP events around each attention launch in the timed steps"
                                 if args.eager else
