@@ -33,11 +33,10 @@
  *   kernels OR bits into it (DAS_DEVERR_*) for out-of-range page ids,
  *   prefix lengths or commit counts, and skip the offending data instead of
  *   reading or writing out of bounds.
- * - Reentrancy: the only global state is a per-device cache of the compute
- *   unit count, filled on first use; calls from several host threads are
- *   safe. Concurrent calls that share a workspace
- *   or write the same cache rows race on the device, as any two kernels
- *   writing the same memory would.
+ * - Reentrancy: the library keeps no global state; calls from several host
+ *   threads are safe. Concurrent calls that share a workspace or write the
+ *   same cache rows race on the device, as any two kernels writing the same
+ *   memory would.
  * - Alignment: the kernels move K/V/Q/O rows with 16-byte accesses, so
  *   k_pool, v_pool, q, k_blk, v_blk, out, k_new and v_new must be 16-byte
  *   aligned (any allocation, or a view starting on a row, is); int32 and
