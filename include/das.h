@@ -134,7 +134,8 @@ typedef struct das_cache {
  */
 typedef struct das_batch {
   int32_t batch;               /* B >= 1                                      */
-  int32_t max_pages_per_seq;   /* columns of block_table, >= 1                */
+  int32_t max_pages_per_seq;   /* columns of block_table, 1..2^24, and
+                                  batch * max_pages_per_seq < 2^31             */
   const int32_t *prefix_len;   /* device [B]                                  */
   const int32_t *block_table;  /* device [B][max_pages_per_seq], int32 pages  */
   uint32_t *dev_error;         /* optional device word (see DAS_DEVERR_*)     */

@@ -42,6 +42,10 @@ das_status check_batch(const das_batch *b) {
   if (!aligned(b->prefix_len, 4) || !aligned(b->block_table, 4) || !aligned(b->dev_error, 4))
     return DAS_ERR_ALIGN;
   if (b->batch < 1 || b->max_pages_per_seq < 1) return DAS_ERR_SHAPE;
+  // positions (pages x 64) and table offsets (B x pages) stay within int32
+  if (b->max_pages_per_seq > (1 << 24) ||
+      static_cast<long long>(b->batch) * b->max_pages_per_seq > 0x7fffffffLL)
+    return DAS_ERR_SHAPE;
   return DAS_OK;
 }
 
