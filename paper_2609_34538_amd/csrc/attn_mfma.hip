@@ -11,7 +11,7 @@
 // XCD, where they share its L2.
 //
 // A chunk fetches its sequence's prefix length, its page ids and its Q rows
-// in one memory round trip, then streams its 32-token tiles (two per prefix
+// (into registers) in one memory round trip, then streams its 32-token tiles (two per prefix
 // page, then the draft block's) through a ring of NB LDS slots filled by the
 // direct-to-LDS loads of gfx950 (global_load_lds_dwordx4), NB tiles ahead
 // of the tile being computed; the loads of the next tile are spread over the
@@ -89,7 +89,7 @@ struct Geo {
   static constexpr int SLOT = NF * kFragBytes;
   static constexpr int NB = NB_;           // ring depth
   static constexpr int QF = NQ * KS;       // Q fragments of a row tile
-  static constexpr int LDS = NB * SLOT + QF * kFragBytes;
+  static constexpr int LDS = NB * SLOT;
 };
 
 template <int DH, int NQ>
@@ -184,7 +184,6 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, i
   constexpr int NF = G::NF;
   constexpr int ROWS = 16 * NQ;
   __shared__ __attribute__((aligned(16))) uint8_t ring[NB * G::SLOT];
-  __shared__ __attribute__((aligned(16))) uint8_t qbuf[G::QF * kFragBytes];
 
   const int lane = threadIdx.x;
   const int ln = lane & 15;
@@ -210,11 +209,14 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, i
   const int b = grp / p.hkv / p.nsplit;
   const int pg0 = split * pps;
 
-  // one round trip: the prefix length, this split's page ids, the Q rows
+  // one round trip: the prefix length, this split's page ids, the Q
+  // fragments (B operand of S^T = K Q^T: lane holds dims 8g..8g+7 of row n,
+  // loaded straight into registers)
   const int s_raw = p.prefix_len[b];
   int page_id = 0;  // lane i: page id of the split's i-th page
   if (lane < pps && pg0 + lane < p.max_pages)
     page_id = p.block_table[static_cast<size_t>(b) * p.max_pages + pg0 + lane];
+  u32x4 qf[NQ][KS];
 #pragma unroll
   for (int qt = 0; qt < NQ; ++qt) {
     // rows past the last are clamped; their outputs are never written
@@ -224,7 +226,7 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, i
                          ((static_cast<size_t>(b) * p.w + i) * p.hq + kvh * p.group + g) * DH;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
-      dma16(qrow + 32 * ks + 8 * lg, qbuf + (qt * KS + ks) * kFragBytes);
+      qf[qt][ks] = *reinterpret_cast<const u32x4 *>(qrow + 32 * ks + 8 * lg);
   }
   bool bad;
   const int S = clamp_prefix(s_raw, p.max_pages, &bad);
@@ -232,10 +234,7 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, i
     report_error(p.dev_error, DAS_DEVERR_PREFIX);
   const int npages = (S + kPage - 1) / kPage;
   const int nsb = max(1, (npages + pps - 1) / pps);  // splits of this sequence
-  if (split >= nsb) {
-    wait_vmcnt<0>();  // the Q rows land in LDS before the workgroup ends
-    return;
-  }
+  if (split >= nsb) return;
   const int npg = max(0, min(pps, npages - pg0));
   const int npg2 = 2 * npg;                                   // prefix tiles
   const int ntile = npg2 + (split == 0 ? (p.w + 31) >> 5 : 0);  // + draft-block tiles
@@ -299,17 +298,9 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, i
   for (; n_issued < NB && n_issued < ntile; ++n_issued)
     for (int part = 0; part < 3; ++part) issue_part(n_issued, part);
 
-  // Q: issued before every tile, so at most n_issued tiles of loads remain
-  wait_tiles<NF>(n_issued);
-  u32x4 qf[NQ][KS];
   int cap_blk[NQ];
 #pragma unroll
-  for (int qt = 0; qt < NQ; ++qt) {
-    cap_blk[qt] = (rt * ROWS + qt * 16 + ln) / p.group;  // block position i of the row
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-      qf[qt][ks] = *reinterpret_cast<const u32x4 *>(qbuf + (qt * KS + ks) * kFragBytes + 16 * lane);
-  }
+  for (int qt = 0; qt < NQ; ++qt) cap_blk[qt] = (rt * ROWS + qt * 16 + ln) / p.group;  // block position i
   State<DH, NQ> st;
 #pragma unroll
   for (int qt = 0; qt < NQ; ++qt) {
