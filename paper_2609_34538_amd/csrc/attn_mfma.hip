@@ -81,6 +81,29 @@ __device__ __forceinline__ f32x4 mfma16x16x32(u32x4 a, u32x4 b, f32x4 c) {
                                                  __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 
+// Reductions over the 4 lanes n, n + 16, n + 32, n + 48 (the rows of the C
+// fragment that hold one query row): gfx950's permlane swaps exchange 16-lane
+// rows (xor 16) and 32-lane halves (xor 32) between two registers in one
+// VALU op, so with both operands = x the pair {x[l], x[l ^ 16]} (or
+// {x[l], x[l ^ 32]}) lands in every lane; max and + are commutative, so the
+// lanes of a group agree bit for bit.
+__device__ __forceinline__ float group_max(float x) {
+  const unsigned u = __float_as_uint(x);
+  const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  const float y = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const unsigned v = __float_as_uint(y);
+  const auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float group_sum(float x) {
+  const unsigned u = __float_as_uint(x);
+  const auto a = __builtin_amdgcn_permlane16_swap(u, u, false, false);
+  const float y = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const unsigned v = __float_as_uint(y);
+  const auto b = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
 template <int DH, int NQ, int NB_>
 struct Geo {
   static constexpr int KS = DH / 32;       // k steps of Q K^T
@@ -139,8 +162,7 @@ __device__ __forceinline__ void compute_tile(State<DH, NQ> &st, const u32x4 (&kf
         mx = fmaxf(mx, x[e][v]);
       }
     }
-    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    mx = group_max(mx);
     const float mnew = fmaxf(st.m[qt], mx);
     const float muse = mnew == kNegInf ? 0.f : mnew;
     alpha[qt] = __builtin_amdgcn_exp2f(st.m[qt] - muse);
@@ -155,8 +177,7 @@ __device__ __forceinline__ void compute_tile(State<DH, NQ> &st, const u32x4 (&kf
         pf[qt][4 * e + v] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(pv));
       }
     }
-    psum += __shfl_xor(psum, 16, 64);
-    psum += __shfl_xor(psum, 32, 64);
+    psum = group_sum(psum);
     st.l[qt] = st.l[qt] * alpha[qt] + psum;
     st.m[qt] = mnew;
   }
