@@ -213,7 +213,9 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, i
 
   // chunk number -> (split group, row tile): in each complete run of 8
   // groups, row tile rt of group 8k + x is number 8 n_rt k + 8 rt + x;
-  // group = (b * nsplit + split) * hkv + kvh
+  // group = (split * B + b) * hkv + kvh, so every sequence's first split is
+  // dispatched before any second split (the longest chunks first: a ragged
+  // batch's short tails come last)
   int grp, rt;
   {
     const int c = blockIdx.x, span = 8 * n_rt, runs = (n_chunks / n_rt) >> 3;
@@ -226,8 +228,8 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, i
     }
   }
   const int kvh = grp % p.hkv;
-  const int split = (grp / p.hkv) % p.nsplit;
-  const int b = grp / p.hkv / p.nsplit;
+  const int b = (grp / p.hkv) % p.batch;
+  const int split = grp / p.hkv / p.batch;
   const int pg0 = split * pps;
 
   // one round trip: the prefix length, this split's page ids, the Q
