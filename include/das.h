@@ -150,7 +150,9 @@ typedef enum das_attn_path {
 
 typedef struct das_attn_options {
   int32_t path;             /* das_attn_path                                 */
-  int32_t pages_per_split;  /* prefix pages per split; 0 = library choice;
+  int32_t pages_per_split;  /* prefix pages per split (the first split of a
+                               sequence, which also takes the draft block,
+                               holds one page less); 0 = library choice;
                                clamped to the block table width, and to 64
                                on the matrix-core path                       */
 } das_attn_options;

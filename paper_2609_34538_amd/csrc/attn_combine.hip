@@ -56,8 +56,7 @@ __global__ __launch_bounds__(64) void attn_combine_kernel(AttnParams p, int skip
   bool bad;
   const int S = clamp_prefix(s_raw, p.max_pages, &bad);
   const int npages = (S + kPage - 1) / kPage;
-  int ns = (npages + p.pages_per_split - 1) / p.pages_per_split;
-  if (ns < 1) ns = 1;
+  const int ns = splits_of(npages, p.pages_per_split);
   if ((ns == 1 && skip_single) || !live) return;  // single split: the attention kernel wrote it
 
   float mx = -__builtin_huge_valf();

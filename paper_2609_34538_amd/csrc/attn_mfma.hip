@@ -230,14 +230,15 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, i
   const int kvh = grp % p.hkv;
   const int b = (grp / p.hkv) % p.batch;
   const int split = grp / p.hkv / p.batch;
-  const int pg0 = split * pps;
+  const int pg0 = split_first_page(split, pps);
+  const int pg_cap = split_first_page(split + 1, pps) - pg0;  // pages of a full split
 
   // one round trip: the prefix length, this split's page ids, the Q
   // fragments (B operand of S^T = K Q^T: lane holds dims 8g..8g+7 of row n,
   // loaded straight into registers)
   const int s_raw = p.prefix_len[b];
   int page_id = 0;  // lane i: page id of the split's i-th page
-  if (lane < pps && pg0 + lane < p.max_pages)
+  if (lane < pg_cap && pg0 + lane < p.max_pages)
     page_id = p.block_table[static_cast<size_t>(b) * p.max_pages + pg0 + lane];
   u32x4 qf[NQ][KS];
 #pragma unroll
@@ -256,9 +257,9 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, i
   if (bad && split == 0 && kvh == 0 && rt == 0 && lane == 0)
     report_error(p.dev_error, DAS_DEVERR_PREFIX);
   const int npages = (S + kPage - 1) / kPage;
-  const int nsb = max(1, (npages + pps - 1) / pps);  // splits of this sequence
+  const int nsb = splits_of(npages, pps);  // splits of this sequence
   if (split >= nsb) return;
-  const int npg = max(0, min(pps, npages - pg0));
+  const int npg = max(0, min(pg_cap, npages - pg0));
   const int npg2 = 2 * npg;                                   // prefix tiles
   const int ntile = npg2 + (split == 0 ? (p.w + 31) >> 5 : 0);  // + draft-block tiles
 

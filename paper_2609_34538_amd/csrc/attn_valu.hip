@@ -54,8 +54,8 @@ __global__ __launch_bounds__(256) void attn_valu_kernel(AttnParams p) {
   if (bad_len && split == 0 && kvh == 0 && rt == 0 && tid == 0)
     report_error(p.dev_error, DAS_DEVERR_PREFIX);
   const int npages = (S + kPage - 1) / kPage;
-  const int pg0 = split * p.pages_per_split;
-  const int pg1 = min(pg0 + p.pages_per_split, npages);
+  const int pg0 = split_first_page(split, p.pages_per_split);
+  const int pg1 = min(split_first_page(split + 1, p.pages_per_split), npages);
   if (split > 0 && pg0 >= pg1) return;  // nothing to do; combine skips it
 
   const int row0 = rt * RT;

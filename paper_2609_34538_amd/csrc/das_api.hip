@@ -102,7 +102,7 @@ das_status make_plan(const das_cache *c, const das_batch *b, int hq, int w,
   if (pps > maxp) pps = maxp;
   if (plan->path == DAS_PATH_MFMA && pps > kMaxPagesPerSplit) pps = kMaxPagesPerSplit;
   plan->pages_per_split = pps;
-  plan->nsplit = (maxp + pps - 1) / pps;
+  plan->nsplit = splits_of(maxp, pps);
   const size_t per_split_rows =
       static_cast<size_t>(b->batch) * c->num_kv_heads * plan->nsplit * plan->rows;
   plan->nsplit_ml = (plan->nsplit + 3) & ~3;

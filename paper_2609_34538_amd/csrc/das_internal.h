@@ -68,6 +68,19 @@ struct AcceptParams {
 };
 hipError_t launch_greedy_accept(const AcceptParams &p, hipStream_t s);
 
+// Prefix split s of a sequence covers its pages [split_first_page(s),
+// split_first_page(s + 1)); split 0 also carries the draft block (at most two
+// 32-token tiles, one page's worth), so it holds one prefix page less and the
+// splits of a sequence do equal work.
+__host__ __device__ __forceinline__ int split_first_page(int s, int pps) {
+  return s == 0 ? 0 : s * pps - 1;
+}
+// Splits of a sequence with `npages` prefix pages: ceil((npages + 1) / pps),
+// at least 1 (the block's).
+__host__ __device__ __forceinline__ int splits_of(int npages, int pps) {
+  return (npages + pps) / pps;
+}
+
 // Query rows of one workgroup of the vector-ALU kernel.
 constexpr int kValuRows = 32;
 

@@ -76,11 +76,12 @@ def test_workspace_size_formula():
     assert ws_bytes(c, b, hq=33) == 0
     assert ws_bytes(c, b, w=0) == 0
     assert ws_bytes(c, b, w=65) == 0
-    # explicit split size: nsplit = ceil(maxp / pps)
+    # explicit split size: nsplit = ceil((maxp + 1) / pps) (the first split also
+    # takes the draft block and holds one page less)
     o = DasOptionsC()
     o.path, o.pages_per_split = 1, 1
     rows, hkv, B, maxp, dh = 8 * 4, 8, 4, 10, 128
-    per = B * hkv * maxp * rows
+    per = B * hkv * (maxp + 1) * rows
     al = lambda x: (x + 255) // 256 * 256
     # partial O per split and row; m and l per row with the splits padded to 4
     assert ws_bytes(c, b, opts=o) == al(per * dh * 4) + 2 * al(B * hkv * rows * 12 * 4)
@@ -93,7 +94,7 @@ def _nsplit_default(B, hkv, maxp, path=2, hq=None, w=8):
     o.path, o.pages_per_split = path, 0
     per_split = B * hkv * w * (hq // hkv)  # rows of one split
     n = ws_bytes(c, b, hq=hq, w=w, opts=o)
-    for ns in range(1, maxp + 1):
+    for ns in range(1, maxp + 2):
         al = lambda x: (x + 255) // 256 * 256
         if al(per_split * ns * 128 * 4) + 2 * al(per_split * ((ns + 3) // 4 * 4) * 4) == n:
             return ns
@@ -101,12 +102,13 @@ def _nsplit_default(B, hkv, maxp, path=2, hq=None, w=8):
 
 
 def test_default_split_rule():
-    # splits = max(2, pow2 floor of 1024 / (B * Hkv * row tiles)), 2 <= pps <= 32
-    assert _nsplit_default(B=16, hkv=8, maxp=200) == 8                # 128 units: pps 25
+    # splits = max(2, pow2 floor of 1024 / (B * Hkv * row tiles)), 2 <= pps <= 32;
+    # split slots = ceil((maxp + 1) / pps)
+    assert _nsplit_default(B=16, hkv=8, maxp=200) == 9                # 128 units: pps 25
     assert _nsplit_default(B=4, hkv=8, maxp=257) == 33                # 32 units: pps 8
     assert _nsplit_default(B=4, hkv=8, maxp=257, hq=32, w=32) == 9    # 4 row tiles: pps 32
     assert _nsplit_default(B=1, hkv=55, maxp=33) == 17                # 55 units: pps 2
-    assert _nsplit_default(B=1, hkv=8, maxp=20) == 10                 # pps 2 (minimum)
+    assert _nsplit_default(B=1, hkv=8, maxp=20) == 11                 # pps 2 (minimum)
     assert _nsplit_default(B=1, hkv=8, maxp=33, path=1) == 17         # same rule on VALU
     assert _nsplit_default(B=32, hkv=8, maxp=1000) == 32              # pps 32 (maximum)
 
