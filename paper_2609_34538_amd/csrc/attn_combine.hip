@@ -40,11 +40,11 @@ __global__ __launch_bounds__(64) void attn_combine_kernel(AttnParams p, int skip
   float4 ov[kEager];
 #pragma unroll
   for (int k4 = 0; k4 < kEager / 4; ++k4) {
-    const bool have = 4 * k4 < p.nsplit_ml;  // uniform
-    const float4 m4 = have ? *reinterpret_cast<const float4 *>(p.ws_m + mbase + 4 * k4)
-                           : make_float4(0.f, 0.f, 0.f, 0.f);
-    const float4 l4 = have ? *reinterpret_cast<const float4 *>(p.ws_l + mbase + 4 * k4)
-                           : make_float4(0.f, 0.f, 0.f, 0.f);
+    // groups past the row's nsplit_ml (a multiple of 4) re-read its last group;
+    // those splits are beyond the count and discarded below
+    const int g4 = min(4 * k4, p.nsplit_ml - 4);
+    const float4 m4 = *reinterpret_cast<const float4 *>(p.ws_m + mbase + g4);
+    const float4 l4 = *reinterpret_cast<const float4 *>(p.ws_l + mbase + g4);
     mv[4 * k4] = m4.x, mv[4 * k4 + 1] = m4.y, mv[4 * k4 + 2] = m4.z, mv[4 * k4 + 3] = m4.w;
     lv[4 * k4] = l4.x, lv[4 * k4 + 1] = l4.y, lv[4 * k4 + 2] = l4.z, lv[4 * k4 + 3] = l4.w;
   }
@@ -53,11 +53,16 @@ __global__ __launch_bounds__(64) void attn_combine_kernel(AttnParams p, int skip
     const size_t r = obase + static_cast<size_t>(k < p.nsplit ? k : 0) * p.rows;
     ov[k] = *reinterpret_cast<const float4 *>(p.ws_o + r * DH + c0);
   }
+  // keep every load above ahead of the first use of its result (one round trip)
+  __builtin_amdgcn_sched_barrier(0);
   bool bad;
   const int S = clamp_prefix(s_raw, p.max_pages, &bad);
   const int npages = (S + kPage - 1) / kPage;
   const int ns = splits_of(npages, p.pages_per_split);
-  if ((ns == 1 && skip_single) || !live) return;  // single split: the attention kernel wrote it
+  // a single split was written by the attention kernel. The merge below runs
+  // regardless and only the stores are skipped, so that the partials' loads
+  // are not deferred behind the prefix length.
+  const bool write = live && !(ns == 1 && skip_single);
 
   float mx = -__builtin_huge_valf();
 #pragma unroll
@@ -75,7 +80,7 @@ __global__ __launch_bounds__(64) void attn_combine_kernel(AttnParams p, int skip
     }
   }
   // splits beyond the first 16, merged in the same online form
-  for (int s0 = kEager; s0 < ns; ++s0) {
+  for (int s0 = kEager; s0 < ns && live; ++s0) {
     const float m = p.ws_m[mbase + s0], l = p.ws_l[mbase + s0];
     const float4 o = *reinterpret_cast<const float4 *>(p.ws_o + (obase + static_cast<size_t>(s0) * p.rows) * DH + c);
     const float nm = fmaxf(mx, m);
@@ -87,6 +92,7 @@ __global__ __launch_bounds__(64) void attn_combine_kernel(AttnParams p, int skip
     n3 = n3 * a + sc * o.w;
     mx = nm;
   }
+  if (!write) return;
   const int i = row / p.group, g = row % p.group;
   const int h = kvh * p.group + g;
   T *out = static_cast<T *>(p.out) + ((static_cast<size_t>(b) * p.w + i) * p.hq + h) * DH + c;
