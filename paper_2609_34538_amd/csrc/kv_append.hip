@@ -9,9 +9,11 @@
 // its n new positions fall in once, then
 //  - keys: copies the n token rows with 16-byte vectors (rows of head_dim
 //    are contiguous in both the source and the token-major page);
-//  - values: stages up to 16 token rows in LDS and writes them into the
-//    token-grouped page ([8][dh][8]) transposed, lanes walking the token
-//    index, so a wave's writes are runs of consecutive 16-byte groups.
+//  - values: stages up to 16 token rows in LDS; then each lane takes one
+//    (head dim, 8-position group) of the token-grouped page ([8][dh][8]),
+//    whose new positions are one contiguous run, and writes the run with
+//    the widest aligned stores that fit it (a full group is one 16-byte
+//    store for bf16).
 // Pure copies: results are bit-exact.
 
 #include "das_internal.h"
@@ -25,6 +27,55 @@ constexpr int kChunk = 16;  // V tokens staged per pass
 struct alignas(16) Vec16 {
   uint32_t x, y, z, w;
 };
+
+// 32-bit words of elements (two bf16 per word, one fp32 per word).
+__device__ __forceinline__ uint32_t word(const bf16_t (&v)[8], int i) {
+  return static_cast<uint32_t>(v[2 * i]) | (static_cast<uint32_t>(v[2 * i + 1]) << 16);
+}
+__device__ __forceinline__ uint32_t word(const float (&v)[8], int i) {
+  return __float_as_uint(v[i]);
+}
+
+// Elements [lo, hi) of an 8-element row (16-byte aligned for bf16, 32 for
+// fp32) from v[], in aligned pieces of at most 16 bytes. Every piece position
+// is a compile-time constant, so v[] stays in registers.
+template <typename T>
+__device__ __forceinline__ void store_run(T *row, const T (&v)[8], int lo, int hi) {
+  constexpr int EPW = 4 / sizeof(T);  // elements per 32-bit word
+  auto inside = [&](int a, int b) { return lo <= a && b <= hi; };
+  if constexpr (sizeof(T) == 2) {
+    if (inside(0, 8)) {
+      *reinterpret_cast<Vec16 *>(row) = Vec16{word(v, 0), word(v, 1), word(v, 2), word(v, 3)};
+      return;
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < 8; q += 4) {
+    if (inside(q, q + 4)) {  // 8 bytes (bf16) or 16 bytes (fp32)
+      const int w0 = q / EPW;
+      if constexpr (sizeof(T) == 2) {
+        *reinterpret_cast<uint2 *>(row + q) = make_uint2(word(v, w0), word(v, w0 + 1));
+      } else {
+        *reinterpret_cast<Vec16 *>(row + q) =
+            Vec16{word(v, w0), word(v, w0 + 1), word(v, w0 + 2), word(v, w0 + 3)};
+      }
+      continue;
+    }
+#pragma unroll
+    for (int e = q; e < q + 4; e += 2) {
+      if (inside(e, e + 2)) {  // 4 bytes (bf16) or 8 bytes (fp32)
+        if constexpr (sizeof(T) == 2) {
+          *reinterpret_cast<uint32_t *>(row + e) = word(v, e / 2);
+        } else {
+          *reinterpret_cast<uint2 *>(row + e) = make_uint2(word(v, e), word(v, e + 1));
+        }
+        continue;
+      }
+      if (inside(e, e + 1)) row[e] = v[e];
+      if (inside(e + 1, e + 2)) row[e + 1] = v[e + 1];
+    }
+  }
+}
 
 template <typename T, int DH>
 __global__ __launch_bounds__(64 * kWaves) void kv_append_kernel(AppendParams p) {
@@ -78,29 +129,28 @@ __global__ __launch_bounds__(64 * kWaves) void kv_append_kernel(AppendParams p) 
     const T *src = static_cast<const T *>(p.k_new) + src_off;
     T *dst = static_cast<T *>(p.k_pool) + dst_head;
     const int total = n * NV;
-    for (int v0 = 0; v0 < total; v0 += 4 * 64) {
-      Vec16 r[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int v = v0 + u * 64 + lane;
-        if (v < total) {
-          const int t = v / NV, c = (v % NV) * VEC;
-          r[u] = *reinterpret_cast<const Vec16 *>(src + t * src_stride + c);
-        }
+    // vector v: token v / NV, columns (v % NV) * VEC ..
+    auto load = [&](int v) {
+      Vec16 r = {0, 0, 0, 0};
+      if (v < total) r = *reinterpret_cast<const Vec16 *>(src + (v / NV) * src_stride + (v % NV) * VEC);
+      return r;
+    };
+    auto store = [&](int v, const Vec16 &r) {
+      if (v >= total) return;
+      const int t = v / NV, c = (v % NV) * VEC;
+      const int pos = S + t;
+      const bool second = pos / kPage != first_page;
+      if (second ? ok1 : ok0) {
+        const size_t page = second ? pg1 : pg0;
+        *reinterpret_cast<Vec16 *>(dst + (page * kPage + pos % kPage) * DH + c) = r;
       }
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int v = v0 + u * 64 + lane;
-        if (v < total) {
-          const int t = v / NV, c = (v % NV) * VEC;
-          const int pos = S + t;
-          const bool second = pos / kPage != first_page;
-          if (second ? ok1 : ok0) {
-            const size_t page = second ? pg1 : pg0;
-            *reinterpret_cast<Vec16 *>(dst + (page * kPage + pos % kPage) * DH + c) = r[u];
-          }
-        }
-      }
+    };
+    for (int v0 = lane; v0 < total; v0 += 4 * 64) {
+      const Vec16 r0 = load(v0), r1 = load(v0 + 64), r2 = load(v0 + 128), r3 = load(v0 + 192);
+      store(v0, r0);
+      store(v0 + 64, r1);
+      store(v0 + 128, r2);
+      store(v0 + 192, r3);
     }
     return;
   }
@@ -121,14 +171,26 @@ __global__ __launch_bounds__(64 * kWaves) void kv_append_kernel(AppendParams p) 
     }
     __syncthreads();
     if (live) {
-      for (int e = lane; e < tc * DH; e += 64) {
-        const int c = e / tc, t = e % tc;
-        const int pos = S + t0 + t;
-        const bool second = pos / kPage != first_page;
-        if (second ? ok1 : ok0) {
-          const size_t page = second ? pg1 : pg0;
-          dst[page * kPage * DH + ((pos % kPage) / 8 * DH + c) * 8 + pos % 8] = st[t * DH + c];
+      // item (dim c, 8-position group gi): the chunk's positions in that group
+      // are one contiguous run of the page's [group][c][8] row, written with
+      // the widest aligned stores that fit it
+      const int p0 = S + t0, p1 = p0 + tc;
+      const int gbase = p0 & ~7;
+      const int ngroups = (p1 - gbase + 7) >> 3;
+      for (int item = lane; item < DH * ngroups; item += 64) {
+        const int c = item % DH, gp = gbase + 8 * (item / DH);
+        const int lo = max(gp, p0), hi = min(gp + 8, p1);
+        const bool second = gp / kPage != first_page;  // 8 | 64: a group lies in one page
+        if (!(second ? ok1 : ok0)) continue;
+        const size_t page = second ? pg1 : pg0;
+        T *row = dst + page * kPage * DH + ((gp % kPage) / 8 * DH + c) * 8;
+        T v[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int t = min(max(gp + j - p0, 0), tc - 1);  // staged token index
+          v[j] = (gp + j >= lo && gp + j < hi) ? st[t * DH + c] : T(0);
         }
+        store_run<T>(row, v, lo - gp, hi - gp);
       }
     }
     __syncthreads();
