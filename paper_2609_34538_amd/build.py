@@ -2,7 +2,8 @@
 
 Run as ``python -m paper_2609_34538_amd.build``. Every call compiles from
 source; the shared library lands next to this file, where the Python binding
-loads it.
+loads it. The compiler's per-kernel resource report (registers, scratch, LDS)
+is written to _build/kernel_resources.txt.
 """
 
 from __future__ import annotations
@@ -10,6 +11,7 @@ from __future__ import annotations
 import concurrent.futures as cf
 import glob
 import os
+import re
 import subprocess
 import sys
 
@@ -19,6 +21,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(PKG, "_build")
 LIB_PATH = os.path.join(PKG, "libdas.so")
+RESOURCES = os.path.join(BUILD_DIR, "kernel_resources.txt")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
@@ -28,20 +31,49 @@ COMMON_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-I", IN
                 "-I", CSRC, "-Wall", "-Wno-unused-function"]
 
 
-def _compile(src: str) -> str:
+def _compile(src: str):
     obj = os.path.join(BUILD_DIR, os.path.basename(src) + ".o")
-    cmd = [HIPCC, *COMMON_FLAGS, *DEVICE_FLAGS, "-c", src, "-o", obj]
+    cmd = [HIPCC, *COMMON_FLAGS, *DEVICE_FLAGS, "-Rpass-analysis=kernel-resource-usage",
+           "-c", src, "-o", obj]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{' '.join(cmd)}\n{res.stdout}{res.stderr}")
-    return obj
+    return obj, _resources(res.stderr)
+
+
+def _resources(report: str):
+    """(kernel, VGPRs, AGPRs, scratch bytes per lane, LDS bytes) from the
+    compiler's kernel-resource-usage remarks."""
+    out, cur = [], None
+    for line in report.splitlines():
+        m = re.search(r"Function Name: (\S+)", line)
+        if m:
+            cur = {"name": m.group(1)}
+            out.append(cur)
+            continue
+        if cur is None:
+            continue
+        for key, pat in (("vgpr", r"\bVGPRs: (\d+)"), ("agpr", r"AGPRs: (\d+)"),
+                         ("scratch", r"ScratchSize \[bytes/lane\]: (\d+)"),
+                         ("lds", r"LDS Size \[bytes/block\]: (\d+)")):
+            m = re.search(pat, line)
+            if m:
+                cur[key] = int(m.group(1))
+    return out
 
 
 def build(verbose: bool = False) -> str:
     os.makedirs(BUILD_DIR, exist_ok=True)
     sources = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
     with cf.ThreadPoolExecutor(max_workers=min(8, len(sources))) as ex:
-        objs = list(ex.map(_compile, sources))
+        results = list(ex.map(_compile, sources))
+    objs = [o for o, _ in results]
+    with open(RESOURCES, "w") as f:
+        f.write("kernel vgpr agpr scratch_bytes_per_lane lds_bytes\n")
+        for _, kernels in results:
+            for k in kernels:
+                f.write(f"{k['name']} {k.get('vgpr', -1)} {k.get('agpr', -1)} "
+                        f"{k.get('scratch', -1)} {k.get('lds', -1)}\n")
     tmp = LIB_PATH + ".tmp"
     cmd = [HIPCC, "-shared", "-fPIC", f"--offload-arch={ARCH}", *objs, "-o", tmp]
     res = subprocess.run(cmd, capture_output=True, text=True)
