@@ -133,7 +133,7 @@ typedef struct das_cache {
  * not exceed 64 * max_pages_per_seq. All three arrays are device memory.
  */
 typedef struct das_batch {
-  int32_t batch;               /* B >= 1                                      */
+  int32_t batch;               /* B, 1..65535                                 */
   int32_t max_pages_per_seq;   /* columns of block_table, 1..2^24, and
                                   batch * max_pages_per_seq < 2^31             */
   const int32_t *prefix_len;   /* device [B]                                  */

@@ -41,7 +41,7 @@ das_status check_batch(const das_batch *b) {
   if (!b->prefix_len || !b->block_table) return DAS_ERR_NULL;
   if (!aligned(b->prefix_len, 4) || !aligned(b->block_table, 4) || !aligned(b->dev_error, 4))
     return DAS_ERR_ALIGN;
-  if (b->batch < 1 || b->max_pages_per_seq < 1) return DAS_ERR_SHAPE;
+  if (b->batch < 1 || b->batch > 65535 || b->max_pages_per_seq < 1) return DAS_ERR_SHAPE;
   // positions (pages x 64) and table offsets (B x pages) stay within int32
   if (b->max_pages_per_seq > (1 << 24) ||
       static_cast<long long>(b->batch) * b->max_pages_per_seq > 0x7fffffffLL)
@@ -103,6 +103,11 @@ das_status make_plan(const das_cache *c, const das_batch *b, int hq, int w,
   if (plan->path == DAS_PATH_MFMA && pps > kMaxPagesPerSplit) pps = kMaxPagesPerSplit;
   plan->pages_per_split = pps;
   plan->nsplit = splits_of(maxp, pps);
+  // workgroups of one launch: (splits x KV heads x row tiles) per sequence
+  const long row_tiles = (plan->rows + 15) / 16;
+  const long wgs = static_cast<long>(b->batch) * c->num_kv_heads * plan->nsplit * row_tiles;
+  if (wgs > 0x7fffffffL || static_cast<long>(b->batch) * row_tiles > 65535)
+    return DAS_ERR_SHAPE;
   const size_t per_split_rows =
       static_cast<size_t>(b->batch) * c->num_kv_heads * plan->nsplit * plan->rows;
   plan->nsplit_ml = (plan->nsplit + 3) & ~3;

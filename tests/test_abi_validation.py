@@ -134,7 +134,7 @@ def test_bad_plane_map_rejected():
 
 @pytest.mark.parametrize("field,value,code", [
     ("batch", 0, SHAPE), ("max_pages_per_seq", 0, SHAPE), ("prefix_len", None, NULL),
-    ("max_pages_per_seq", (1 << 24) + 1, SHAPE), ("batch", 1 << 28, SHAPE),
+    ("max_pages_per_seq", (1 << 24) + 1, SHAPE), ("batch", 1 << 28, SHAPE), ("batch", 65536, SHAPE),
     ("block_table", None, NULL), ("prefix_len", FAKE + 2, ALIGN),
     ("block_table", FAKE + 1, ALIGN), ("dev_error", FAKE + 2, ALIGN),
 ])
