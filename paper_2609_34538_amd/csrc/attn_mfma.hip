@@ -2,7 +2,8 @@
 //
 // One single-wave workgroup per chunk = (sequence, KV head, row tile of
 // 16 * NQ query rows, prefix split of up to pages_per_split pages); split 0
-// of every (sequence, head, row tile) also carries the draft block. The grid
+// of every (sequence, head, row tile) also carries the draft block, in place
+// of one prefix page, so every split streams the same number of tiles. The grid
 // holds every chunk the block table's width allows; a chunk past its
 // sequence's prefix exits at once, and the hardware dispatcher keeps the
 // compute units fed as chunks finish. Workgroups are dealt to the 8 XCDs
