@@ -14,11 +14,13 @@
 // A chunk fetches its sequence's prefix length, its page ids and its Q rows
 // (into registers) in one memory round trip, then streams its 32-token tiles (two per prefix
 // page, then the draft block's) through a ring of NB LDS slots filled by the
-// direct-to-LDS loads of gfx950 (global_load_lds_dwordx4), NB tiles ahead
-// of the tile being computed; the loads of the next tile are spread over the
+// direct-to-LDS loads of gfx950 (buffer_load_dwordx4 ... lds for prefix
+// pages, global_load_lds_dwordx4 for the draft block), NB tiles ahead of the
+// tile being computed; the loads of the next tile are spread over the
 // computation of the current one. The wave waits on its own vector-memory
-// counter for the data it reads. Load addresses are a uniform base (page,
-// fragment) plus one per-lane offset.
+// counter for the data it reads. A prefix tile's loads address a buffer
+// resource per page half with one per-lane offset and a uniform fragment
+// offset in an SGPR.
 //
 // Both products run on v_mfma_f32_16x16x32_bf16 with the key/value tile as
 // the A operand, so softmax probabilities never leave registers:
@@ -38,7 +40,8 @@
 // A chunk ends by writing its (m, l, O) partial to the workspace for the
 // combine kernel, or, when its sequence has a single split, the normalised
 // output. Query rows of a row tile: row = i * G + g (block position i,
-// head kvh * G + g). Logits are scaled into base-2 units after the product.
+// head kvh * G + g). Logits are scaled into base-2 units after the product,
+// inside the exponent's fused multiply-add.
 
 #include "das_internal.h"
 
@@ -58,6 +61,21 @@ constexpr int kFragBytes = 64 * 16;  // one 16-byte fragment per lane
 __device__ __forceinline__ void dma16(const void *src, uint8_t *lds) {
   __builtin_amdgcn_global_load_lds((__attribute__((address_space(1))) void *)(src),
                                    (__attribute__((address_space(3))) void *)(lds), 16, 0, 0);
+}
+
+// Raw buffer resource over `bytes` bytes at `base` (stride 0; word 3 = the
+// gfx9 raw-buffer format). Out-of-range lanes read zeros.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_of(const void *base, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, bytes, 0x00020000);
+}
+
+// 16 bytes per lane from resource r at byte voff (per lane) + soff (uniform)
+// -> LDS at lds + 16 * lane. The uniform part travels in an SGPR, so a
+// fragment costs no vector address arithmetic.
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, uint32_t voff, int soff,
+                                      uint8_t *lds) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void *)(lds),
+                                           16, voff, soff, 0, 0);
 }
 
 // s_waitcnt vmcnt(n), other counters untouched (gfx9 encoding).
@@ -122,6 +140,12 @@ struct State {
   f32x4 o[NQ][DH / 16];
 };
 
+// A row's softmax reference m (base-2 units) moves only when a tile's maximum
+// exceeds it by more than kLazy, so that the accumulators are rarely rescaled;
+// probabilities 2^(x - m) then stay <= 2^kLazy. Softmax is invariant under the
+// choice of reference, so only rounding differs from the running-maximum form.
+constexpr float kLazy = 8.f;
+
 // One 32-token tile through both products and the online softmax. Token t of
 // the tile (0..31) is visible when t < limit and t <= cap[qt]; a full tile
 // (every token visible) skips the mask.
@@ -138,19 +162,23 @@ __device__ __forceinline__ void compute_tile(State<DH, NQ> &st, const u32x4 (&kf
   bool moved = false;
   f32x4 sacc[NQ][2];
   hook(0);
+  // k-step outermost: the 2 * NQ accumulators are independent, so no MFMA
+  // waits for the one before it
 #pragma unroll
-  for (int qt = 0; qt < NQ; ++qt) {
+  for (int qt = 0; qt < NQ; ++qt)
 #pragma unroll
-    for (int e = 0; e < 2; ++e) {
-      sacc[qt][e] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int e = 0; e < 2; ++e) sacc[qt][e] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int ks = 0; ks < DH / 32; ++ks)
-        sacc[qt][e] = mfma16x16x32(kf[e][ks], qf[qt][ks], sacc[qt][e]);
-    }
-  }
+  for (int ks = 0; ks < DH / 32; ++ks)
+#pragma unroll
+    for (int qt = 0; qt < NQ; ++qt)
+#pragma unroll
+      for (int e = 0; e < 2; ++e) sacc[qt][e] = mfma16x16x32(kf[e][ks], qf[qt][ks], sacc[qt][e]);
   hook(1);
 #pragma unroll
   for (int qt = 0; qt < NQ; ++qt) {
+    // raw logits; masked ones are -inf. scale > 0, so the maximum of the
+    // scaled logits is the scaled maximum.
     float x[2][4];
     float mx = kNegInf;
 #pragma unroll
@@ -159,31 +187,33 @@ __device__ __forceinline__ void compute_tile(State<DH, NQ> &st, const u32x4 (&kf
       for (int v = 0; v < 4; ++v) {
         const int t = 8 * lg + 4 * e + v;
         const bool vis = full || ((t < limit) & (t <= cap[qt]));
-        x[e][v] = vis ? sacc[qt][e][v] * scale : kNegInf;
+        x[e][v] = vis ? sacc[qt][e][v] : kNegInf;
         mx = fmaxf(mx, x[e][v]);
       }
     }
-    mx = group_max(mx);
-    const float mnew = fmaxf(st.m[qt], mx);
-    const float muse = mnew == kNegInf ? 0.f : mnew;
-    alpha[qt] = __builtin_amdgcn_exp2f(st.m[qt] - muse);
-    moved |= alpha[qt] != 1.f;
+    mx = group_max(mx) * scale;
+    // -inf + kLazy = -inf: the first visible tile always sets the reference
+    const bool up = mx > st.m[qt] + kLazy;
+    const float mref = up ? mx : st.m[qt];
+    alpha[qt] = up ? __builtin_amdgcn_exp2f(st.m[qt] - mref) : 1.f;
+    moved |= up;
+    const float neg = mref == kNegInf ? 0.f : -mref;  // nothing visible yet: every p is 0
     float psum = 0.f;
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
-        const float pv = __builtin_amdgcn_exp2f(x[e][v] - muse);
+        const float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(x[e][v], scale, neg));
         psum += pv;
         pf[qt][4 * e + v] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(pv));
       }
     }
     psum = group_sum(psum);
     st.l[qt] = st.l[qt] * alpha[qt] + psum;
-    st.m[qt] = mnew;
+    st.m[qt] = mref;
   }
   hook(2);
-  // rescale the accumulators only when some row's maximum moved
+  // rescale the accumulators only when some row's reference moved
   if (__builtin_amdgcn_ballot_w64(moved) != 0) {
 #pragma unroll
     for (int qt = 0; qt < NQ; ++qt)
@@ -278,27 +308,34 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, i
   const uint32_t lane_k = ((8 * (ln >> 2) + (ln & 3)) * DH + 8 * lg) * 2;
   const uint32_t lane_v = (lg * DH + ln) * 16;
 
+  // Source of prefix tile t: its page's 32-token key half ([32][DH], at
+  // kbase) and value half (token groups 4u .. 4u + 3 of [8][DH][8], at vbase),
+  // resolved once per tile. An out-of-range page id is reported and read as
+  // page 0 (its tile is masked out).
+  auto tile_src = [&](int t, const char *&kbase, const char *&vbase) {
+    const int page = __builtin_amdgcn_readlane(page_id, t >> 1);
+    const bool ok = page >= 0 && page < p.num_pages;
+    if (!ok) report_error(p.dev_error, DAS_DEVERR_PAGE);
+    const size_t off = head_off + static_cast<size_t>(ok ? page : 0) * kPage * DH * 2;
+    const int u = t & 1;
+    kbase = kl + off + (32 * u) * DH * 2;
+    vbase = vl + off + 64 * DH * u;
+  };
   // Loads of tile t into ring slot t % NB, in three parts (key fragments of
   // each S^T half, then the values) so they can be spread over the
-  // computation of the previous tile.
-  auto issue_part = [&](int t, int part) {
+  // computation of the previous tile. Both halves span 64 * DH bytes.
+  auto issue_part = [&](int t, int part, const char *kbase, const char *vbase) {
     uint8_t *slot = ring + (t % NB) * G::SLOT;
     if (t < npg2) {
-      const int page = __builtin_amdgcn_readlane(page_id, t >> 1);
-      const bool ok = page >= 0 && page < p.num_pages;
-      if (part == 0 && !ok) report_error(p.dev_error, DAS_DEVERR_PAGE);
-      const size_t off = head_off + static_cast<size_t>(ok ? page : 0) * kPage * DH * 2;
-      const int u = t & 1;
       if (part < 2) {
-        const char *kb = kl + off + (32 * u) * DH * 2;
+        const auto r = buffer_of(kbase, 64 * DH);
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
-          dma16(kb + (4 * part * DH + 32 * ks) * 2 + lane_k, slot + (part * KS + ks) * kFragBytes);
+          dma16(r, lane_k, (4 * part * DH + 32 * ks) * 2, slot + (part * KS + ks) * kFragBytes);
       } else {
-        const char *vb = vl + off + 64 * DH * u;  // token groups 4u .. 4u + 3
+        const auto r = buffer_of(vbase, 64 * DH);
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt)
-          dma16(vb + 256 * dt + lane_v, slot + (2 * KS + dt) * kFragBytes);
+        for (int dt = 0; dt < DT; ++dt) dma16(r, lane_v, 256 * dt, slot + (2 * KS + dt) * kFragBytes);
       }
     } else {
       // draft block tile u: key fragments by token slot, value rows raw
@@ -320,8 +357,11 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, i
   };
 
   int n_issued = 0;
-  for (; n_issued < NB && n_issued < ntile; ++n_issued)
-    for (int part = 0; part < 3; ++part) issue_part(n_issued, part);
+  for (; n_issued < NB && n_issued < ntile; ++n_issued) {
+    const char *kbase = kl, *vbase = vl;
+    if (n_issued < npg2) tile_src(n_issued, kbase, vbase);
+    for (int part = 0; part < 3; ++part) issue_part(n_issued, part, kbase, vbase);
+  }
 
   int cap_blk[NQ];
 #pragma unroll
@@ -378,8 +418,10 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, i
     const int next = n_issued;
     const bool refill = next < ntile;
     if (refill) ++n_issued;
+    const char *kbase = kl, *vbase = vl;
+    if (refill && next < npg2) tile_src(next, kbase, vbase);
     compute_tile<DH, NQ>(st, kf, vf, qf, cap, limit, full, p.scale_log2, lg, [&](int part) {
-      if (refill) issue_part(next, part);
+      if (refill) issue_part(next, part, kbase, vbase);
     });
   }
 
