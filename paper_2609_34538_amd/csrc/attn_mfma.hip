@@ -140,12 +140,6 @@ struct State {
   f32x4 o[NQ][DH / 16];
 };
 
-// A row's softmax reference m (base-2 units) moves only when a tile's maximum
-// exceeds it by more than kLazy, so that the accumulators are rarely rescaled;
-// probabilities 2^(x - m) then stay <= 2^kLazy. Softmax is invariant under the
-// choice of reference, so only rounding differs from the running-maximum form.
-constexpr float kLazy = 8.f;
-
 // One 32-token tile through both products and the online softmax. Token t of
 // the tile (0..31) is visible when t < limit and t <= cap[qt]; a full tile
 // (every token visible) skips the mask.
@@ -180,24 +174,32 @@ __device__ __forceinline__ void compute_tile(State<DH, NQ> &st, const u32x4 (&kf
     // raw logits; masked ones are -inf. scale > 0, so the maximum of the
     // scaled logits is the scaled maximum.
     float x[2][4];
-    float mx = kNegInf;
 #pragma unroll
-    for (int e = 0; e < 2; ++e) {
+    for (int e = 0; e < 2; ++e)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int t = 8 * lg + 4 * e + v;
-        const bool vis = full || ((t < limit) & (t <= cap[qt]));
-        x[e][v] = vis ? sacc[qt][e][v] : kNegInf;
-        mx = fmaxf(mx, x[e][v]);
+      for (int v = 0; v < 4; ++v) x[e][v] = sacc[qt][e][v];
+    if (!full) {  // uniform: a full tile skips the mask
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int t = 8 * lg + 4 * e + v;
+          x[e][v] = ((t < limit) & (t <= cap[qt])) ? x[e][v] : kNegInf;
+        }
       }
     }
+    float mx = kNegInf;
+#pragma unroll
+    for (int e = 0; e < 2; ++e)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) mx = fmaxf(mx, x[e][v]);
+    // Running maximum (base-2 units): the row's largest probability is
+    // exactly 1 and those near it fall just below, where bf16 rounds finest.
     mx = group_max(mx) * scale;
-    // -inf + kLazy = -inf: the first visible tile always sets the reference
-    const bool up = mx > st.m[qt] + kLazy;
-    const float mref = up ? mx : st.m[qt];
-    alpha[qt] = up ? __builtin_amdgcn_exp2f(st.m[qt] - mref) : 1.f;
-    moved |= up;
-    const float neg = mref == kNegInf ? 0.f : -mref;  // nothing visible yet: every p is 0
+    const float mnew = fmaxf(st.m[qt], mx);
+    const float neg = mnew == kNegInf ? 0.f : -mnew;  // nothing visible yet: every p is 0
+    alpha[qt] = __builtin_amdgcn_exp2f(st.m[qt] + neg);
+    moved |= alpha[qt] != 1.f;
     float psum = 0.f;
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
@@ -210,10 +212,10 @@ __device__ __forceinline__ void compute_tile(State<DH, NQ> &st, const u32x4 (&kf
     }
     psum = group_sum(psum);
     st.l[qt] = st.l[qt] * alpha[qt] + psum;
-    st.m[qt] = mref;
+    st.m[qt] = mnew;
   }
   hook(2);
-  // rescale the accumulators only when some row's reference moved
+  // rescale the accumulators only when some row's maximum moved
   if (__builtin_amdgcn_ballot_w64(moved) != 0) {
 #pragma unroll
     for (int qt = 0; qt < NQ; ++qt)
@@ -228,8 +230,12 @@ __device__ __forceinline__ void compute_tile(State<DH, NQ> &st, const u32x4 (&kf
   }
 }
 
+// At least two waves per SIMD: the kernel then fits in 256 registers, so the
+// output and score accumulators stay in VGPRs (the MFMAs write them there)
+// instead of being copied out of AGPRs on every tile.
 template <int DH, int NQ, int NB>
-__global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, int n_chunks) {
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2)))
+void attn_mfma_kernel(AttnParams p, int n_rt, int n_chunks) {
   using G = Geo<DH, NQ, NB>;
   constexpr int KS = G::KS;
   constexpr int DT = G::DT;
@@ -290,6 +296,12 @@ __global__ __launch_bounds__(64) void attn_mfma_kernel(AttnParams p, int n_rt, i
   const int npages = (S + kPage - 1) / kPage;
   const int nsb = splits_of(npages, pps);  // splits of this sequence
   if (split >= nsb) return;
+  // The round trip's loads (prefix length, page ids, Q fragments) are done
+  // before any tile load is issued: the page ids are needed at once, and with
+  // no load into registers left pending, the loop's waits count tile loads
+  // only (otherwise a use of those registers inside the loop has to wait for
+  // every load issued before it, prefetched tiles included).
+  wait_vmcnt<0>();
   const int npg = max(0, min(pg_cap, npages - pg0));
   const int npg2 = 2 * npg;                                   // prefix tiles
   const int ntile = npg2 + (split == 0 ? (p.w + 31) >> 5 : 0);  // + draft-block tiles
