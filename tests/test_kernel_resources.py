@@ -30,3 +30,14 @@ def test_no_scratch_and_lds_within_limits():
         assert scratch == 0, f"{name} uses {scratch} bytes of scratch per lane"
         assert 0 <= lds <= 160 * 1024, f"{name} uses {lds} bytes of LDS"
         assert 0 <= vgpr <= 512 and 0 <= agpr <= 256, name
+
+
+def test_attention_kernels_keep_accumulators_in_vgprs():
+    """The matrix-core kernel is built for two waves per SIMD, which keeps it
+    within 256 registers with no AGPRs: above that budget the MFMAs wrote the
+    accumulators to AGPRs and every tile copied them back (64 moves per tile
+    at head dim 128)."""
+    mfma = [k for k in _kernels() if "attn_mfma_kernel" in k[0]]
+    assert mfma
+    for name, vgpr, agpr, scratch, lds in mfma:
+        assert agpr == 0 and vgpr <= 256, f"{name}: {vgpr} VGPRs, {agpr} AGPRs"
