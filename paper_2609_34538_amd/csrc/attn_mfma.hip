@@ -241,11 +241,7 @@ void attn_mfma_kernel(AttnParams p, int n_rt, int n_chunks) {
   constexpr int DT = G::DT;
   constexpr int NF = G::NF;
   constexpr int ROWS = 16 * NQ;
-  // NB * G::SLOT bytes, sized at launch: with the ring out of the static
-  // LDS size the compiler keeps its two-waves-per-SIMD register budget for
-  // every ring depth (a static 48 KB ring reads as at most one wave per SIMD
-  // and brings the AGPR copies back)
-  extern __shared__ __attribute__((aligned(16))) uint8_t ring[];
+  __shared__ __attribute__((aligned(16))) uint8_t ring[NB * G::SLOT];
 
   const int lane = threadIdx.x;
   const int ln = lane & 15;
@@ -485,25 +481,15 @@ hipError_t launch_typed(const AttnParams &p, hipStream_t s) {
   // every possible chunk (the table width bounds the splits of a sequence)
   const long chunks = static_cast<long>(p.batch) * p.hkv * p.nsplit * n_rt;
   if (chunks > 0x7fffffffL) return hipErrorInvalidValue;
-  constexpr unsigned lds = Geo<DH, NQ, NB>::LDS;  // the ring
   hipLaunchKernelGGL((attn_mfma_kernel<DH, NQ, NB>), dim3(static_cast<unsigned>(chunks)),
-                     dim3(64), lds, s, p, n_rt, static_cast<int>(chunks));
+                     dim3(64), 0, s, p, n_rt, static_cast<int>(chunks));
   return hipGetLastError();
 }
 
-// Ring depth: chunks of 16+ pages at head dim <= 96 keep 4 tiles in flight
-// (a long chunk's time is its own stream's latency-bound rate; 3 resident
-// chunks per CU at dh 96); shorter chunks and dh 128 keep 2, so that more
-// chunks are resident (short chunks are all start-up; at dh 128 a deeper ring
-// would leave 2 chunks per CU and the row tiles of a split no longer share
-// the L2).
 template <int DH>
 hipError_t launch_dh(const AttnParams &p, hipStream_t s) {
-  if constexpr (DH <= 96) {
-    if (p.pages_per_split >= 16)
-      return p.rows <= 16 ? launch_typed<DH, 1, 4>(p, s) : launch_typed<DH, 2, 4>(p, s);
-  }
-  return p.rows <= 16 ? launch_typed<DH, 1, 2>(p, s) : launch_typed<DH, 2, 2>(p, s);
+  if (p.rows <= 16) return launch_typed<DH, 1, 2>(p, s);
+  return launch_typed<DH, 2, 2>(p, s);
 }
 
 }  // namespace
