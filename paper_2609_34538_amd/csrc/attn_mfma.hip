@@ -1,7 +1,10 @@
 // Matrix-core (MFMA) policy-attention kernel for bf16 caches (Eq. (2)-(3)).
 //
-// One single-wave workgroup per chunk = (sequence, KV head, row tile of
-// 16 * NQ query rows, prefix split of up to pages_per_split pages); split 0
+// One wave per chunk = (sequence, KV head, row tile of 16 * NQ query rows,
+// prefix split of up to pages_per_split pages). Blocks of up to 32 query rows
+// run one single-wave workgroup per chunk; larger (GQA) blocks run the 2 or 4
+// row tiles of a split as the waves of one workgroup that share one LDS ring,
+// so a tile is loaded once per split rather than once per row tile. Split 0
 // of every (sequence, head, row tile) also carries the draft block, in place
 // of one prefix page, so every split streams the same number of tiles. The grid
 // holds every chunk the block table's width allows; a chunk past its
@@ -233,9 +236,14 @@ __device__ __forceinline__ void compute_tile(State<DH, NQ> &st, const u32x4 (&kf
 // At least two waves per SIMD: the kernel then fits in 256 registers, so the
 // output and score accumulators stay in VGPRs (the MFMAs write them there)
 // instead of being copied out of AGPRs on every tile.
-template <int DH, int NQ, int NB>
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2)))
-void attn_mfma_kernel(AttnParams p, int n_rt, int n_chunks) {
+// NW = 1: one wave per chunk, its own ring. NW > 1: the NW row tiles of a
+// split share one workgroup and one ring; each wave loads every NW-th
+// fragment of a tile and one barrier per tile both publishes the tile and
+// frees the slot read in the previous iteration, which is then refilled
+// (NB - 1 tiles in flight).
+template <int DH, int NQ, int NB, int NW>
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2)))
+void attn_mfma_kernel(AttnParams p, int n_rg, int n_chunks) {
   using G = Geo<DH, NQ, NB>;
   constexpr int KS = G::KS;
   constexpr int DT = G::DT;
@@ -243,27 +251,30 @@ void attn_mfma_kernel(AttnParams p, int n_rt, int n_chunks) {
   constexpr int ROWS = 16 * NQ;
   __shared__ __attribute__((aligned(16))) uint8_t ring[NB * G::SLOT];
 
-  const int lane = threadIdx.x;
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
   const int ln = lane & 15;
   const int lg = lane >> 4;
   const int pps = p.pages_per_split;
 
-  // chunk number -> (split group, row tile): in each complete run of 8
-  // groups, row tile rt of group 8k + x is number 8 n_rt k + 8 rt + x;
+  // chunk number -> (split group, row-tile group of NW row tiles): in each
+  // complete run of 8 groups, row-tile group rg of group 8k + x is number
+  // 8 n_rg k + 8 rg + x;
   // group = (split * B + b) * hkv + kvh, so every sequence's first split is
   // dispatched before any second split (the longest chunks first: a ragged
   // batch's short tails come last)
-  int grp, rt;
+  int grp, rg;
   {
-    const int c = blockIdx.x, span = 8 * n_rt, runs = (n_chunks / n_rt) >> 3;
+    const int c = blockIdx.x, span = 8 * n_rg, runs = (n_chunks / n_rg) >> 3;
     if (c < runs * span) {
       grp = 8 * (c / span) + (c % span & 7);
-      rt = (c % span) >> 3;
+      rg = (c % span) >> 3;
     } else {
-      grp = c / n_rt;
-      rt = c % n_rt;
+      grp = c / n_rg;
+      rg = c % n_rg;
     }
   }
+  const int rt = rg * NW + wave;  // this wave's row tile
   const int kvh = grp % p.hkv;
   const int b = (grp / p.hkv) % p.batch;
   const int split = grp / p.hkv / p.batch;
@@ -333,6 +344,8 @@ void attn_mfma_kernel(AttnParams p, int n_rt, int n_chunks) {
     kbase = kl + off + (32 * u) * DH * 2;
     vbase = vl + off + 64 * DH * u;
   };
+  // fragment f of a tile is loaded by wave f % NW
+  auto mine = [&](int f) { return NW == 1 || f % NW == wave; };
   // Loads of tile t into ring slot t % NB, in three parts (key fragments of
   // each S^T half, then the values) so they can be spread over the
   // computation of the previous tile. Both halves span 64 * DH bytes.
@@ -343,11 +356,13 @@ void attn_mfma_kernel(AttnParams p, int n_rt, int n_chunks) {
         const auto r = buffer_of(kbase, 64 * DH);
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
-          dma16(r, lane_k, (4 * part * DH + 32 * ks) * 2, slot + (part * KS + ks) * kFragBytes);
+          if (mine(part * KS + ks))
+            dma16(r, lane_k, (4 * part * DH + 32 * ks) * 2, slot + (part * KS + ks) * kFragBytes);
       } else {
         const auto r = buffer_of(vbase, 64 * DH);
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) dma16(r, lane_v, 256 * dt, slot + (2 * KS + dt) * kFragBytes);
+        for (int dt = 0; dt < DT; ++dt)
+          if (mine(2 * KS + dt)) dma16(r, lane_v, 256 * dt, slot + (2 * KS + dt) * kFragBytes);
       }
     } else {
       // draft block tile u: key fragments by token slot, value rows raw
@@ -356,10 +371,12 @@ void attn_mfma_kernel(AttnParams p, int n_rt, int n_chunks) {
         const int tok = min(32 * u + 8 * (ln >> 2) + 4 * part + (ln & 3), p.w - 1);
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
-          dma16(kblk + tok * tok_bytes + (32 * ks + 8 * lg) * 2, slot + (part * KS + ks) * kFragBytes);
+          if (mine(part * KS + ks))
+            dma16(kblk + tok * tok_bytes + (32 * ks + 8 * lg) * 2, slot + (part * KS + ks) * kFragBytes);
       } else {
 #pragma unroll
         for (int f = 0; f < DT; ++f) {
+          if (!mine(2 * KS + f)) continue;
           const int o = f * kFragBytes + 16 * lane;  // byte in the [32][DH] half
           const int tok = min(32 * u + o / (2 * DH), p.w - 1);
           dma16(vblk + tok * tok_bytes + o % (2 * DH), slot + (2 * KS + f) * kFragBytes);
@@ -387,6 +404,7 @@ void attn_mfma_kernel(AttnParams p, int n_rt, int n_chunks) {
     for (int dt = 0; dt < DT; ++dt) st.o[qt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
+  if constexpr (NW == 1) {
   for (int t = 0; t < ntile; ++t) {
     wait_tiles<NF>(n_issued - t - 1);
     const uint8_t *slot = ring + (t % NB) * G::SLOT;
@@ -437,6 +455,61 @@ void attn_mfma_kernel(AttnParams p, int n_rt, int n_chunks) {
     });
   }
 
+  } else {
+  for (int t = 0; t < ntile; ++t) {
+    wait_tiles<NF / NW>(n_issued - t - 1);  // this wave's loads of tile t have landed
+    // every wave's loads of tile t have landed, and every wave has read slot
+    // (t - 1) % NB, which now takes tile t - 1 + NB
+    __syncthreads();
+    if (t >= 1 && n_issued < ntile) {
+      const char *kbase = kl, *vbase = vl;
+      if (n_issued < npg2) tile_src(n_issued, kbase, vbase);
+      for (int part = 0; part < 3; ++part) issue_part(n_issued, part, kbase, vbase);
+      ++n_issued;
+    }
+    const uint8_t *slot = ring + (t % NB) * G::SLOT;
+    u32x4 kf[2][KS], vf[DT];
+#pragma unroll
+    for (int e = 0; e < 2; ++e)
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+        kf[e][ks] = *reinterpret_cast<const u32x4 *>(slot + (e * KS + ks) * kFragBytes + 16 * lane);
+    int cap[NQ];
+    int limit;
+    bool full;
+    if (t < npg2) {
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+        vf[dt] = *reinterpret_cast<const u32x4 *>(slot + (2 * KS + dt) * kFragBytes + 16 * lane);
+      const int page = __builtin_amdgcn_readlane(page_id, t >> 1);
+      const bool ok = page >= 0 && page < p.num_pages;
+      limit = ok ? min(32, S - (pg0 + (t >> 1)) * kPage - 32 * (t & 1)) : 0;
+      full = limit >= 32;
+#pragma unroll
+      for (int qt = 0; qt < NQ; ++qt) cap[qt] = 0x7fffffff;
+    } else {
+      // block values are token-major [32][DH] in the slot: gather V^T
+      const int u = t - npg2;
+      const uint16_t *raw = reinterpret_cast<const uint16_t *>(slot + 2 * KS * kFragBytes);
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        u16x8 v8;
+#pragma unroll
+        for (int jj = 0; jj < 8; ++jj) v8[jj] = raw[(8 * lg + jj) * DH + 16 * dt + ln];
+        vf[dt] = __builtin_bit_cast(u32x4, v8);
+      }
+      limit = p.w - 32 * u;
+      full = false;
+#pragma unroll
+      for (int qt = 0; qt < NQ; ++qt) cap[qt] = cap_blk[qt] - 32 * u;
+    }
+    // the slot's fragments are in registers before the next barrier
+    __builtin_amdgcn_s_waitcnt(0xF | (0x3 << 14) | (0x7 << 4));  // lgkmcnt(0)
+    compute_tile<DH, NQ>(st, kf, vf, qf, cap, limit, full, p.scale_log2, lg, [](int) {});
+  }
+
+  }
+
   // Chunk result. Lane holds head dims 16dt + 4g .. +3 of row n of tile qt.
   const size_t prow0 = ((static_cast<size_t>(b) * p.hkv + kvh) * p.nsplit + split) * p.rows;
 #pragma unroll
@@ -475,21 +548,30 @@ void attn_mfma_kernel(AttnParams p, int n_rt, int n_chunks) {
   }
 }
 
-template <int DH, int NQ, int NB>
+template <int DH, int NQ, int NB, int NW>
 hipError_t launch_typed(const AttnParams &p, hipStream_t s) {
   const int n_rt = (p.rows + 16 * NQ - 1) / (16 * NQ);
+  const int n_rg = (n_rt + NW - 1) / NW;  // row-tile groups (workgroups) per split
   // every possible chunk (the table width bounds the splits of a sequence)
-  const long chunks = static_cast<long>(p.batch) * p.hkv * p.nsplit * n_rt;
+  const long chunks = static_cast<long>(p.batch) * p.hkv * p.nsplit * n_rg;
   if (chunks > 0x7fffffffL) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((attn_mfma_kernel<DH, NQ, NB>), dim3(static_cast<unsigned>(chunks)),
-                     dim3(64), 0, s, p, n_rt, static_cast<int>(chunks));
+  hipLaunchKernelGGL((attn_mfma_kernel<DH, NQ, NB, NW>), dim3(static_cast<unsigned>(chunks)),
+                     dim3(64 * NW), 0, s, p, n_rg, static_cast<int>(chunks));
   return hipGetLastError();
 }
 
+// Up to 32 query rows: one wave per chunk. More rows (GQA blocks): the row
+// tiles of a split share a workgroup and one ring, so each tile enters LDS
+// once per split instead of once per row tile. Four row tiles and more: four
+// waves and a 4-deep ring (two workgroups per CU; long-prefix GQA 0.33 ->
+// 0.41 of HBM peak); two row tiles: two waves and a 2-deep ring (a 4-deep
+// one would leave one wave per SIMD at head dim 128).
 template <int DH>
 hipError_t launch_dh(const AttnParams &p, hipStream_t s) {
-  if (p.rows <= 16) return launch_typed<DH, 1, 2>(p, s);
-  return launch_typed<DH, 2, 2>(p, s);
+  if (p.rows <= 16) return launch_typed<DH, 1, 2, 1>(p, s);
+  if (p.rows <= 32) return launch_typed<DH, 2, 2, 1>(p, s);
+  if (p.rows <= 64) return launch_typed<DH, 2, 2, 2>(p, s);
+  return launch_typed<DH, 2, 4, 4>(p, s);
 }
 
 }  // namespace

@@ -92,8 +92,11 @@ das_status make_plan(const das_cache *c, const das_batch *b, int hq, int w,
     const long tile_rows = plan->path == DAS_PATH_MFMA ? (plan->rows <= 16 ? 16 : 32) : kValuRows;
     const long units = static_cast<long>(b->batch) * c->num_kv_heads *
                        ((plan->rows + tile_rows - 1) / tile_rows);
+    // matrix-core blocks of more than 32 rows run their row tiles as the
+    // waves of one workgroup (two per CU): they take twice the row-tile chunks
+    const long target = plan->path == DAS_PATH_MFMA && plan->rows > 32 ? 2048 : 1024;
     long splits = 2;
-    while (splits * 2 * units <= 1024) splits *= 2;
+    while (splits * 2 * units <= target) splits *= 2;
     long want = maxp / splits;
     if (want < 2) want = 2;
     if (want > 32) want = 32;

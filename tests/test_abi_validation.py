@@ -102,11 +102,13 @@ def _nsplit_default(B, hkv, maxp, path=2, hq=None, w=8):
 
 
 def test_default_split_rule():
-    # splits = max(2, pow2 floor of 1024 / (B * Hkv * row tiles)), 2 <= pps <= 32;
-    # split slots = ceil((maxp + 1) / pps)
+    # splits = max(2, pow2 floor of T / (B * Hkv * row tiles)), 2 <= pps <= 32,
+    # T = 1024, or 2048 for matrix-core blocks of more than 32 rows (their row
+    # tiles share a workgroup); split slots = ceil((maxp + 1) / pps)
     assert _nsplit_default(B=16, hkv=8, maxp=200) == 9                # 128 units: pps 25
     assert _nsplit_default(B=4, hkv=8, maxp=257) == 33                # 32 units: pps 8
-    assert _nsplit_default(B=4, hkv=8, maxp=257, hq=32, w=32) == 9    # 4 row tiles: pps 32
+    assert _nsplit_default(B=4, hkv=8, maxp=257, hq=32, w=32) == 17   # 4 row tiles: pps 16
+    assert _nsplit_default(B=4, hkv=8, maxp=257, hq=16, w=32) == 33   # 2 row tiles: pps 8
     assert _nsplit_default(B=1, hkv=55, maxp=33) == 17                # 55 units: pps 2
     assert _nsplit_default(B=1, hkv=8, maxp=20) == 11                 # pps 2 (minimum)
     assert _nsplit_default(B=1, hkv=8, maxp=33, path=1) == 17         # same rule on VALU
