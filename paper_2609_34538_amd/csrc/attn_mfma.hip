@@ -425,6 +425,19 @@ void attn_mfma_kernel(AttnParams p, int n_rg, int n_chunks) {
       const bool ok = page >= 0 && page < p.num_pages;
       limit = ok ? min(32, S - (pg0 + (t >> 1)) * kPage - 32 * (t & 1)) : 0;
       full = limit >= 32;
+      if (!full) {
+        // Invisible tokens (past the prefix, or an unreadable page) enter P.V
+        // with probability 0; their values are zeroed so that whatever the
+        // cache holds there (NaN, Inf) contributes nothing. Lane group lg
+        // holds tokens 8 lg .. 8 lg + 7 of the tile, two per 32-bit word.
+        const int nv = min(max(limit - 8 * lg, 0), 8);
+        u32x4 keep;
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+          keep[k] = (2 * k < nv ? 0xffffu : 0u) | (2 * k + 1 < nv ? 0xffff0000u : 0u);
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) vf[dt] &= keep;
+      }
 #pragma unroll
       for (int qt = 0; qt < NQ; ++qt) cap[qt] = 0x7fffffff;
     } else {
@@ -485,6 +498,19 @@ void attn_mfma_kernel(AttnParams p, int n_rg, int n_chunks) {
       const bool ok = page >= 0 && page < p.num_pages;
       limit = ok ? min(32, S - (pg0 + (t >> 1)) * kPage - 32 * (t & 1)) : 0;
       full = limit >= 32;
+      if (!full) {
+        // Invisible tokens (past the prefix, or an unreadable page) enter P.V
+        // with probability 0; their values are zeroed so that whatever the
+        // cache holds there (NaN, Inf) contributes nothing. Lane group lg
+        // holds tokens 8 lg .. 8 lg + 7 of the tile, two per 32-bit word.
+        const int nv = min(max(limit - 8 * lg, 0), 8);
+        u32x4 keep;
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+          keep[k] = (2 * k < nv ? 0xffffu : 0u) | (2 * k + 1 < nv ? 0xffff0000u : 0u);
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) vf[dt] &= keep;
+      }
 #pragma unroll
       for (int qt = 0; qt < NQ; ++qt) cap[qt] = 0x7fffffff;
     } else {

@@ -112,12 +112,15 @@ __global__ __launch_bounds__(256) void attn_valu_kernel(AttnParams p) {
       bool ok = page >= 0 && page < p.num_pages;
       if (!ok && tid == 0) report_error(p.dev_error, DAS_DEVERR_PAGE);
       const size_t base = kvh * head_elems + static_cast<size_t>(ok ? page : 0) * kPage * DH;
+      // tokens past the prefix (and an unreadable page) are staged as zeros:
+      // they enter P.V with probability 0, whatever the cache holds there
+      const int valid = ok ? min(kPage, S - tile * kPage) : 0;
       for (int e = tid; e < kPage * DH; e += 256) {
         // key tile is [64][DH], value tile is [8][DH][8]; both contiguous
         const int j = e / DH, c = e % DH;
-        sK[j * KS + c] = ok ? to_f32<T>(kl[base + e]) : 0.f;
+        sK[j * KS + c] = j < valid ? to_f32<T>(kl[base + e]) : 0.f;
         const int cv = (e >> 3) % DH, jv = 8 * (e / (8 * DH)) + (e & 7);
-        sV[cv * VS + jv] = ok ? to_f32<T>(vl[base + e]) : 0.f;
+        sV[cv * VS + jv] = jv < valid ? to_f32<T>(vl[base + e]) : 0.f;
       }
       if (!ok) ntok = 0;  // skip the unreadable page
     }

@@ -171,3 +171,36 @@ def test_long_prefix_split_sizes(pps):
     torch.cuda.synchronize()
     ref, _ = oracle_call(cd, 0, 2, wl.depth_R, q, kb, vb, range(wl.batch))
     assert_close(out, ref, wl.dtype, f"long prefix pps={pps}")
+
+
+def _poison_past_prefix(cd: dg.CacheData):
+    """Fill every cache slot past a sequence's prefix in its last page with
+    NaN (keys) and Inf / NaN (values), in every plane and layer."""
+    for b, s_len in enumerate(cd.prefix_lens):
+        s_len = int(s_len)
+        if s_len % dg.PAGE == 0:
+            continue
+        page = int(cd.block_table[b][s_len // dg.PAGE])
+        for t in range(s_len % dg.PAGE, dg.PAGE):
+            cd.k_pool[:, :, :, page, t, :] = float("nan")
+            cd.v_pool[:, :, :, page, t // 8, :, t % 8] = float("inf") if t % 2 else float("nan")
+
+
+@pytest.mark.parametrize("name,path", [("c3s", "valu"), ("c3s", "mfma"), ("c1", "valu"),
+                                       ("gqa8_w32", "mfma"), ("c5s", "mfma")])
+def test_non_finite_cache_past_the_prefix_is_ignored(name, path):
+    """Positions past a sequence's prefix enter the softmax with probability
+    0; whatever the cache holds there (here NaN and Inf) must contribute
+    nothing, so the output still matches the oracle, which reads only the
+    prefix."""
+    wl = small_workloads()[name]
+    torch.manual_seed(0)
+    cd = dg.make_cache(wl, DEV, prefix_lens=EDGE_LENS.get(name))
+    _poison_past_prefix(cd)
+    cache, batch = wrap(cd)
+    d, w = wl.draft_depths[-1], wl.draft_widths[-1]
+    q, kb, vb = dg.block_inputs(cd, w, d, DEV)
+    out = das.attn_policy(cache, batch, 0, d, wl.depth_R, q, kb, vb, **KERNELS[path])
+    torch.cuda.synchronize()
+    ref, _ = oracle_call(cd, 0, d, wl.depth_R, q, kb, vb, range(wl.batch))
+    assert_close(out, ref, wl.dtype, f"{name} {path} with non-finite cache past the prefix")
