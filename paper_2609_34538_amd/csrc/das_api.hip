@@ -89,7 +89,8 @@ das_status make_plan(const das_cache *c, const das_batch *b, int hq, int w,
   const int maxp = b->max_pages_per_seq;
   int pps = o ? o->pages_per_split : 0;
   if (pps == 0) {
-    const long tile_rows = plan->path == DAS_PATH_MFMA ? (plan->rows <= 16 ? 16 : 32) : kValuRows;
+    const long tile_rows = plan->path == DAS_PATH_MFMA ? (plan->rows <= 16 ? 16 : 32)
+                                                      : valu_tile_rows(plan->rows);
     const long units = static_cast<long>(b->batch) * c->num_kv_heads *
                        ((plan->rows + tile_rows - 1) / tile_rows);
     // matrix-core blocks of more than 32 rows run their row tiles as the

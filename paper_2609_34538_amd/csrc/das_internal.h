@@ -81,8 +81,11 @@ __host__ __device__ __forceinline__ int splits_of(int npages, int pps) {
   return (npages + pps) / pps;
 }
 
-// Query rows of one workgroup of the vector-ALU kernel.
-constexpr int kValuRows = 32;
+// Query rows of one workgroup of the vector-ALU kernel: the smallest of 4, 8,
+// 16 that holds the block's rows, else 32 (several row tiles).
+__host__ __device__ constexpr int valu_tile_rows(int rows) {
+  return rows <= 4 ? 4 : rows <= 8 ? 8 : rows <= 16 ? 16 : 32;
+}
 
 // ---------------------------------------------------------------------------
 // Device helpers

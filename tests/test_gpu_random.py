@@ -53,3 +53,26 @@ def test_random_shapes(seed):
                 f"w={w} lens={lens} pps={pps} ({kappa},{nu})")
         assert_close(out, ref, wl.dtype, what)
         assert_lse_close(lse, ref_lse, what)
+
+
+@pytest.mark.parametrize("seed", range(100, 124))
+def test_random_shapes_fp32(seed):
+    """fp32 caches (vector-ALU kernel only) at every head dim and block width,
+    so every row-tile size of that kernel (4, 8, 16, 32 rows) is met."""
+    wl, lens, pps, rng = _case(seed)
+    wl = dg.scaled(wl, dtype=torch.float32)
+    torch.manual_seed(seed)
+    cd = dg.make_cache(wl, DEV, prefix_lens=lens)
+    cache, batch = wrap(cd)
+    R = wl.depth_R
+    kappa, nu = int(rng.integers(1, R + 1)), int(rng.integers(1, R + 1))
+    w = wl.draft_widths[0]
+    q, kb, vb = dg.block_inputs(cd, w, kappa, DEV)
+    ref, ref_lse = oracle_call(cd, 1, kappa, nu, q, kb, vb, range(wl.batch))
+    lse = torch.empty((wl.batch, wl.hq, w), dtype=torch.float32, device=DEV)
+    out = das.attn_policy(cache, batch, 1, kappa, nu, q, kb, vb, lse=lse, pages_per_split=pps)
+    torch.cuda.synchronize()
+    what = (f"seed {seed} fp32: B={wl.batch} Hkv={wl.hkv} G={wl.group} dh={wl.dh} "
+            f"w={w} lens={lens} pps={pps} ({kappa},{nu})")
+    assert_close(out, ref, wl.dtype, what)
+    assert_lse_close(lse, ref_lse, what)
