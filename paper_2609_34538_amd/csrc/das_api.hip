@@ -94,12 +94,15 @@ das_status make_plan(const das_cache *c, const das_batch *b, int hq, int w,
     const long units = static_cast<long>(b->batch) * c->num_kv_heads *
                        ((plan->rows + tile_rows - 1) / tile_rows);
     // matrix-core blocks of more than 32 rows run their row tiles as the
-    // waves of one workgroup (two per CU): they take twice the row-tile chunks
-    const long target = plan->path == DAS_PATH_MFMA && plan->rows > 32 ? 2048 : 1024;
+    // waves of one workgroup (two per CU): they take twice the row-tile
+    // chunks. Vector-ALU workgroups are four waves holding 37-94 KB of LDS
+    // (one to four per CU): half the chunks, and a split may be one page.
+    const bool mfma = plan->path == DAS_PATH_MFMA;
+    const long target = mfma ? (plan->rows > 32 ? 2048 : 1024) : 512;
     long splits = 2;
     while (splits * 2 * units <= target) splits *= 2;
     long want = maxp / splits;
-    if (want < 2) want = 2;
+    if (want < (mfma ? 2 : 1)) want = mfma ? 2 : 1;
     if (want > 32) want = 32;
     pps = static_cast<int>(want);
   }

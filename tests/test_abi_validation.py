@@ -111,7 +111,10 @@ def test_default_split_rule():
     assert _nsplit_default(B=4, hkv=8, maxp=257, hq=16, w=32) == 33   # 2 row tiles: pps 8
     assert _nsplit_default(B=1, hkv=55, maxp=33) == 17                # 55 units: pps 2
     assert _nsplit_default(B=1, hkv=8, maxp=20) == 11                 # pps 2 (minimum)
-    assert _nsplit_default(B=1, hkv=8, maxp=33, path=1) == 17         # same rule on VALU
+    # vector-ALU kernel: T = 512 and splits of 1..32 pages
+    assert _nsplit_default(B=1, hkv=8, maxp=33, path=1) == 34         # 8 units: pps 1
+    assert _nsplit_default(B=1, hkv=55, maxp=32, path=1) == 9         # 55 units: pps 4
+    assert _nsplit_default(B=16, hkv=8, maxp=200, path=1) == 7        # 128 units: pps 32
     assert _nsplit_default(B=32, hkv=8, maxp=1000) == 32              # pps 32 (maximum)
 
 
