@@ -159,10 +159,12 @@ def test_all_read_policies(small_data):
         assert_close(out, ref, wl.dtype, f"policy ({kappa},{nu})")
 
 
-@pytest.mark.parametrize("pps", [0, 63, 64, 100])
+@pytest.mark.parametrize("pps", [0, 1, 3, 5, 63, 64, 100])
 def test_long_prefix_split_sizes(pps):
     """Splits longer than 64 pages are clamped; a 5000-token prefix spans 79
-    pages, so every clamp and the last partial split are exercised."""
+    pages, so every clamp and the last partial split are exercised. 1, 3 and
+    5 pages give 80, 27 and 16 splits: the merge's eager loads of 16 and 32
+    splits and its serial tail past 32."""
     wl = dg.scaled(W[5], batch=3, hq=2, hkv=2, layers=1, prefix=(4000, 5000))
     cd = dg.make_cache(wl, DEV, prefix_lens=[5000, 4100, 64 * 64])
     cache, batch = wrap(cd)
