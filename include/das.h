@@ -153,8 +153,10 @@ typedef struct das_attn_options {
   int32_t pages_per_split;  /* prefix pages per split (the first split of a
                                sequence, which also takes the draft block,
                                holds one page less); 0 = library choice;
-                               clamped to the block table width, and to 64
-                               on the matrix-core path                       */
+                               clamped to the block table width + 1 (one
+                               split then holds any sequence, and no merge
+                               kernel runs), and to 64 on the matrix-core
+                               path                                          */
 } das_attn_options;
 
 /*

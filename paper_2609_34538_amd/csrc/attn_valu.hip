@@ -12,8 +12,8 @@
 // broadcast probability chunks); every LDS read moves 16 bytes. The next
 // tile's global loads are issued into registers before the current tile's
 // arithmetic. Row max / sum are wave reductions over DPP and permlane swaps.
-// The unnormalised partial (O, m, l) goes to the workspace; the combine
-// kernel merges splits.
+// The unnormalised partial (O, m, l) goes to the workspace and the combine
+// kernel merges splits; a sequence that fits one split is written directly.
 
 #include "das_internal.h"
 
@@ -104,6 +104,7 @@ __global__ __launch_bounds__(256) void attn_valu_kernel(AttnParams p) {
   if (bad_len && split == 0 && kvh == 0 && rt == 0 && tid == 0)
     report_error(p.dev_error, DAS_DEVERR_PREFIX);
   const int npages = (S + kPage - 1) / kPage;
+  const int nsb = splits_of(npages, p.pages_per_split);  // this sequence's splits
   const int pg0 = split_first_page(split, p.pages_per_split);
   const int pg1 = min(split_first_page(split + 1, p.pages_per_split), npages);
   if (split > 0 && pg0 >= pg1) return;  // nothing to do; combine skips it
@@ -269,12 +270,28 @@ __global__ __launch_bounds__(256) void attn_valu_kernel(AttnParams p) {
     }
   }
 
-  // Unnormalised partial results of this split.
+  // A sequence with a single split is normalised and written here (split 0
+  // holds the block's diagonal, so l > 0); otherwise the unnormalised partial
+  // of this split goes to the workspace for the combine kernel.
 #pragma unroll
   for (int k = 0; k < RW; ++k) {
     const int r = wave + 4 * k;
     if (r >= nrows) continue;
     const int row = row0 + r;
+    if (nsb == 1) {
+      const float inv = 1.f / l[k];
+      const int i = row / p.group, h = kvh * p.group + row % p.group;
+      T *orow = static_cast<T *>(p.out) + ((static_cast<size_t>(b) * p.w + i) * p.hq + h) * DH;
+#pragma unroll
+      for (int c = 0; c < NC; ++c) {
+        const int col = lane + 64 * c;
+        if (col < DH) orow[col] = from_f32<T>(acc[k][c] * inv);
+      }
+      if (lane == 0 && p.lse)
+        p.lse[(static_cast<size_t>(b) * p.hq + h) * p.w + i] =
+            (m[k] + log2f(l[k])) * 0.69314718055994530942f;
+      continue;
+    }
     const size_t prow = (((static_cast<size_t>(b) * p.hkv + kvh) * p.nsplit + split) * p.rows + row);
 #pragma unroll
     for (int c = 0; c < NC; ++c) {

@@ -106,7 +106,8 @@ das_status make_plan(const das_cache *c, const das_batch *b, int hq, int w,
     if (want > 32) want = 32;
     pps = static_cast<int>(want);
   }
-  if (pps > maxp) pps = maxp;
+  // at most maxp + 1 pages: one split then holds any sequence and its block
+  if (pps > maxp + 1) pps = maxp + 1;
   if (plan->path == DAS_PATH_MFMA && pps > kMaxPagesPerSplit) pps = kMaxPagesPerSplit;
   plan->pages_per_split = pps;
   plan->nsplit = splits_of(maxp, pps);
@@ -187,7 +188,9 @@ das_status attn_common(const das_cache *c, const das_batch *b, int layer, int ka
   const hipError_t e = mfma ? launch_attn_mfma(p, dh, stream)
                             : launch_attn_valu(p, c->dtype, dh, stream);
   if (e != hipSuccess) return DAS_ERR_HIP;
-  if (launch_attn_combine(p, c->dtype, dh, mfma ? 1 : 0, stream) != hipSuccess) return DAS_ERR_HIP;
+  // one split per sequence: the attention kernel wrote every output itself
+  if (plan.nsplit > 1 && launch_attn_combine(p, c->dtype, dh, 1, stream) != hipSuccess)
+    return DAS_ERR_HIP;
   return DAS_OK;
 }
 

@@ -53,7 +53,7 @@ struct AppendParams {
 hipError_t launch_attn_valu(const AttnParams &p, int dtype, int dh, hipStream_t s);
 hipError_t launch_attn_mfma(const AttnParams &p, int dh, hipStream_t s);
 // skip_single: sequences whose prefix fits one split were already written
-// by the attention kernel (matrix-core path).
+// by the attention kernel (both kernel families write them directly).
 hipError_t launch_attn_combine(const AttnParams &p, int dtype, int dh, int skip_single,
                                hipStream_t s);
 hipError_t launch_kv_append(const AppendParams &p, int dtype, int dh, hipStream_t s);
