@@ -92,11 +92,15 @@ def test_split_sizes_agree_with_oracle(small_data, path, pps):
     wl = cd.wl
     cache, batch = wrap(cd)
     q, kb, vb = dg.block_inputs(cd, 16, 2, DEV)
-    out = das.attn_policy(cache, batch, 1, 2, wl.depth_R, q, kb, vb, pages_per_split=pps,
+    lse = torch.empty((wl.batch, wl.hq, 16), dtype=torch.float32, device=DEV)
+    out = das.attn_policy(cache, batch, 1, 2, wl.depth_R, q, kb, vb, lse=lse, pages_per_split=pps,
                           **KERNELS[path])
     torch.cuda.synchronize()
-    ref, _ = oracle_call(cd, 1, 2, wl.depth_R, q, kb, vb, range(wl.batch))
+    ref, ref_lse = oracle_call(cd, 1, 2, wl.depth_R, q, kb, vb, range(wl.batch))
+    # pps = 100: one split per sequence, outputs and lse written by the
+    # attention kernel itself, no merge kernel
     assert_close(out, ref, wl.dtype, f"pps={pps} {path}")
+    assert_lse_close(lse, ref_lse, f"pps={pps} {path} lse")
 
 
 @pytest.mark.parametrize("path", list(KERNELS))
