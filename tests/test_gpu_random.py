@@ -33,7 +33,7 @@ def _case(seed):
     return wl, lens, pps, rng
 
 
-@pytest.mark.parametrize("seed", range(24))
+@pytest.mark.parametrize("seed", range(128))
 def test_random_shapes(seed):
     wl, lens, pps, rng = _case(seed)
     torch.manual_seed(seed)
@@ -55,7 +55,7 @@ def test_random_shapes(seed):
         assert_lse_close(lse, ref_lse, what)
 
 
-@pytest.mark.parametrize("seed", range(100, 124))
+@pytest.mark.parametrize("seed", range(1000, 1128))
 def test_random_shapes_fp32(seed):
     """fp32 caches (vector-ALU kernel only) at every head dim and block width,
     so every row-tile size of that kernel (4, 8, 16, 32 rows) is met."""
