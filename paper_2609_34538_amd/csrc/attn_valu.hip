@@ -99,30 +99,36 @@ __global__ __launch_bounds__(256) void attn_valu_kernel(AttnParams p) {
   const int b = blockIdx.z / n_rt;
   const int rt = blockIdx.z % n_rt;
 
-  bool bad_len;
-  const int S = clamp_prefix(p.prefix_len[b], p.max_pages, &bad_len);
-  if (bad_len && split == 0 && kvh == 0 && rt == 0 && tid == 0)
-    report_error(p.dev_error, DAS_DEVERR_PREFIX);
-  const int npages = (S + kPage - 1) / kPage;
-  const int nsb = splits_of(npages, p.pages_per_split);  // this sequence's splits
-  const int pg0 = split_first_page(split, p.pages_per_split);
-  const int pg1 = min(split_first_page(split + 1, p.pages_per_split), npages);
-  if (split > 0 && pg0 >= pg1) return;  // nothing to do; combine skips it
-
   const int row0 = rt * RT;
   const int nrows = min(RT, p.rows - row0);
+  const int pg0 = split_first_page(split, p.pages_per_split);
+  const int first_tile = (split == 0) ? -1 : pg0;  // -1 = the draft block
+  const int32_t *table = p.block_table + static_cast<size_t>(b) * p.max_pages;
+  // page id of a prefix tile (-1 past the table); its address does not
+  // depend on the prefix length
+  auto page_of = [&](int tile) { return tile >= 0 && tile < p.max_pages ? table[tile] : -1; };
+
+  // One memory round trip before any arithmetic: the prefix length, the page
+  // ids of the split's first two tiles and this row tile's Q are read
+  // together, and the first tile's K/V follow its page id without waiting
+  // for the prefix length. Every address stays in bounds whatever the length
+  // turns out to be (a split past the prefix exits below).
+  const int s_raw = p.prefix_len[b];
+  int pid_cur = page_of(first_tile), pid_nxt = page_of(first_tile + 1);
+  constexpr int QPT = (RT * DH + 255) / 256;  // Q elements per thread
   const T *q = static_cast<const T *>(p.q);
-  // Q rows of this tile, pre-scaled into base-2 logit units.
-  for (int e = tid; e < RT * DH; e += 256) {
+  float qv[QPT];
+#pragma unroll
+  for (int u = 0; u < QPT; ++u) {
+    const int e = u * 256 + tid;
     const int r = e / DH, c = e % DH;
-    float v = 0.f;
-    if (r < nrows) {
+    qv[u] = 0.f;
+    if (e < RT * DH && r < nrows) {
       const int row = row0 + r;
       const int i = row / p.group, g = row % p.group;
       const size_t off = ((static_cast<size_t>(b) * p.w + i) * p.hq + kvh * p.group + g) * DH + c;
-      v = to_f32<T>(q[off]) * p.scale_log2;
+      qv[u] = to_f32<T>(q[off]);
     }
-    sQ[e] = v;
   }
 
   const T *kl = static_cast<const T *>(p.k_layer);
@@ -130,16 +136,13 @@ __global__ __launch_bounds__(256) void attn_valu_kernel(AttnParams p) {
   const T *kb = static_cast<const T *>(p.kb);
   const T *vb = static_cast<const T *>(p.vb);
   const size_t head_elems = static_cast<size_t>(p.num_pages) * kPage * DH;
-  const int first_tile = (split == 0) ? -1 : pg0;  // -1 = the draft block
 
   // Thread tid's chunks of a tile are u * 256 + tid, u < NL: chunk e holds
   // elements 4e .. 4e + 3 of the key tile [64][DH] and of the value tile
   // ([8][DH][8] for a page, [w][Hkv][DH] rows for the draft block).
   Raw4<T> rk[NL], rv[NL];
-  int valid_next = 0;  // tokens of the loaded tile that are visible (else zero)
-  auto load_tile = [&](int tile) {
+  auto load_tile = [&](int tile, int page) {
     if (tile < 0) {
-      valid_next = p.w;
 #pragma unroll
       for (int u = 0; u < NL; ++u) {
         const int e = u * 256 + tid;
@@ -154,12 +157,8 @@ __global__ __launch_bounds__(256) void attn_valu_kernel(AttnParams p) {
         }
       }
     } else {
-      const int page = p.block_table[static_cast<size_t>(b) * p.max_pages + tile];
+      // an unreadable page id reads page 0; its tokens are staged as zeros
       const bool ok = page >= 0 && page < p.num_pages;
-      if (!ok && tid == 0) report_error(p.dev_error, DAS_DEVERR_PAGE);
-      // tokens past the prefix (and an unreadable page) are staged as zeros:
-      // they enter P.V with probability 0, whatever the cache holds there
-      valid_next = ok ? min(kPage, S - tile * kPage) : 0;
       const size_t base = kvh * head_elems + static_cast<size_t>(ok ? page : 0) * kPage * DH;
 #pragma unroll
       for (int u = 0; u < NL; ++u) {
@@ -169,6 +168,24 @@ __global__ __launch_bounds__(256) void attn_valu_kernel(AttnParams p) {
       }
     }
   };
+  load_tile(first_tile, pid_cur);
+
+  bool bad_len;
+  const int S = clamp_prefix(s_raw, p.max_pages, &bad_len);
+  if (bad_len && split == 0 && kvh == 0 && rt == 0 && tid == 0)
+    report_error(p.dev_error, DAS_DEVERR_PREFIX);
+  const int npages = (S + kPage - 1) / kPage;
+  const int nsb = splits_of(npages, p.pages_per_split);  // this sequence's splits
+  const int pg1 = min(split_first_page(split + 1, p.pages_per_split), npages);
+  if (split > 0 && pg0 >= pg1) return;  // nothing to do; combine skips it
+
+  // Q rows of this tile, pre-scaled into base-2 logit units.
+#pragma unroll
+  for (int u = 0; u < QPT; ++u) {
+    const int e = u * 256 + tid;
+    if (e < RT * DH) sQ[e] = qv[u] * p.scale_log2;
+  }
+
   auto store_tile = [&](bool is_block, int valid) {
 #pragma unroll
     for (int u = 0; u < NL; ++u) {
@@ -205,14 +222,22 @@ __global__ __launch_bounds__(256) void attn_valu_kernel(AttnParams p) {
     for (int c = 0; c < NC; ++c) acc[k][c] = 0.f;
   }
 
-  load_tile(first_tile);
   for (int tile = first_tile; tile < pg1; ++tile) {
     const bool is_block = tile < 0;
-    const int ntok = valid_next;
+    const bool ok = pid_cur >= 0 && pid_cur < p.num_pages;
+    if (!is_block && !ok && tid == 0) report_error(p.dev_error, DAS_DEVERR_PAGE);
+    // visible tokens of this tile: the block's w, a page's tokens before the
+    // prefix length (none for an unreadable page); the rest are staged as zeros
+    const int ntok = is_block ? p.w : (ok ? min(kPage, S - tile * kPage) : 0);
     __syncthreads();  // previous tile fully consumed (and sQ written)
     store_tile(is_block, ntok);
     __syncthreads();
-    if (tile + 1 < pg1) load_tile(tile + 1);  // in flight during this tile
+    // the page id two tiles ahead and the next tile's K/V are in flight
+    // during this tile
+    const int pid_after = page_of(tile + 2);
+    if (tile + 1 < pg1) load_tile(tile + 1, pid_nxt);
+    pid_cur = pid_nxt;
+    pid_nxt = pid_after;
 
     // Logits: lane = token j, this wave's RW rows.
     const int j = lane;
