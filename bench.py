@@ -43,7 +43,7 @@ HBM_PEAK_GBS = 8000.0
 # FETCH_SIZE / WRITE_SIZE passes over this benchmark's default command, each
 # scaled by what the counter reads for a plain 1 GiB copy; valid only for the
 # kernel sources with this digest, the default workload and library plan.
-MEASURED_TRAFFIC = {("single-seq-looped-bf16", "84a75bedd8e2c9af"): 50_916_277}
+MEASURED_TRAFFIC = {("single-seq-looped-bf16", "0a7531cfff422980"): 47_904_779}
 TRAFFIC_SOURCES = ["paper_2609_34538_amd/csrc/attn_mfma.hip",
                    "paper_2609_34538_amd/csrc/attn_combine.hip",
                    "paper_2609_34538_amd/csrc/das_api.hip",

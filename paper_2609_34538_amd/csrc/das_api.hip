@@ -93,12 +93,13 @@ das_status make_plan(const das_cache *c, const das_batch *b, int hq, int w,
                                                       : valu_tile_rows(plan->rows);
     const long units = static_cast<long>(b->batch) * c->num_kv_heads *
                        ((plan->rows + tile_rows - 1) / tile_rows);
-    // matrix-core blocks of more than 32 rows run their row tiles as the
-    // waves of one workgroup (two per CU): they take twice the row-tile
-    // chunks. Vector-ALU workgroups are four waves holding 37-94 KB of LDS
-    // (one to four per CU): half the chunks, and a split may be one page.
+    // about two chunks per CU: longer chunks amortise their first round
+    // trip and leave fewer partials to merge. Matrix-core blocks of more than
+    // 32 rows run their row tiles as the waves of one workgroup (two per CU):
+    // they take four times the row-tile chunks. On the vector-ALU path a
+    // split may be one page.
     const bool mfma = plan->path == DAS_PATH_MFMA;
-    const long target = mfma ? (plan->rows > 32 ? 2048 : 1024) : 512;
+    const long target = mfma && plan->rows > 32 ? 2048 : 512;
     long splits = 2;
     while (splits * 2 * units <= target) splits *= 2;
     long want = maxp / splits;

@@ -103,15 +103,15 @@ def _nsplit_default(B, hkv, maxp, path=2, hq=None, w=8):
 
 def test_default_split_rule():
     # splits = max(2, pow2 floor of T / (B * Hkv * row tiles)), 2 <= pps <= 32,
-    # T = 1024, or 2048 for matrix-core blocks of more than 32 rows (their row
+    # T = 512, or 2048 for matrix-core blocks of more than 32 rows (their row
     # tiles share a workgroup); split slots = ceil((maxp + 1) / pps)
-    assert _nsplit_default(B=16, hkv=8, maxp=200) == 9                # 128 units: pps 25
-    assert _nsplit_default(B=4, hkv=8, maxp=257) == 33                # 32 units: pps 8
+    assert _nsplit_default(B=16, hkv=8, maxp=200) == 7                # 128 units: pps 32
+    assert _nsplit_default(B=4, hkv=8, maxp=257) == 17                # 32 units: pps 16
     assert _nsplit_default(B=4, hkv=8, maxp=257, hq=32, w=32) == 17   # 4 row tiles: pps 16
     assert _nsplit_default(B=4, hkv=8, maxp=257, hq=16, w=32) == 33   # 2 row tiles: pps 8
-    assert _nsplit_default(B=1, hkv=55, maxp=33) == 17                # 55 units: pps 2
+    assert _nsplit_default(B=1, hkv=55, maxp=33) == 9                 # 55 units: pps 4
     assert _nsplit_default(B=1, hkv=8, maxp=20) == 11                 # pps 2 (minimum)
-    # vector-ALU kernel: T = 512 and splits of 1..32 pages
+    # vector-ALU kernel: the same T = 512, and splits of 1..32 pages
     assert _nsplit_default(B=1, hkv=8, maxp=33, path=1) == 34         # 8 units: pps 1
     assert _nsplit_default(B=1, hkv=55, maxp=32, path=1) == 9         # 55 units: pps 4
     assert _nsplit_default(B=16, hkv=8, maxp=200, path=1) == 7        # 128 units: pps 32
