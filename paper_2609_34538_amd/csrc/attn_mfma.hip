@@ -126,6 +126,19 @@ __device__ __forceinline__ float group_sum(float x) {
   return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
+// Issue priority of a long chunk from the tiles it has left: among the
+// chunks resident on a CU, the one with more work left issues first, so the
+// long chunks of a ragged batch do not run alone at the end of the launch.
+// Short chunks keep the hardware's oldest-first order, which measured better
+// when the chunks are of equal length.
+constexpr int kLongChunkTiles = 40;
+__device__ __forceinline__ void prio_by_remaining(int rem) {
+  if (rem > 24) __builtin_amdgcn_s_setprio(3);
+  else if (rem > 12) __builtin_amdgcn_s_setprio(2);
+  else if (rem > 4) __builtin_amdgcn_s_setprio(1);
+  else __builtin_amdgcn_s_setprio(0);
+}
+
 template <int DH, int NQ, int NB_>
 struct Geo {
   static constexpr int KS = DH / 32;       // k steps of Q K^T
@@ -405,7 +418,9 @@ void attn_mfma_kernel(AttnParams p, int n_rg, int n_chunks) {
   }
 
   if constexpr (NW == 1) {
+  const bool long_chunk = ntile > kLongChunkTiles;
   for (int t = 0; t < ntile; ++t) {
+    if (long_chunk) prio_by_remaining(ntile - t);
     wait_tiles<NF>(n_issued - t - 1);
     const uint8_t *slot = ring + (t % NB) * G::SLOT;
     u32x4 kf[2][KS], vf[DT];
