@@ -43,7 +43,7 @@ HBM_PEAK_GBS = 8000.0
 # FETCH_SIZE / WRITE_SIZE passes over this benchmark's default command, each
 # scaled by what the counter reads for a plain 1 GiB copy; valid only for the
 # kernel sources with this digest, the default workload and library plan.
-MEASURED_TRAFFIC = {("single-seq-looped-bf16", "d2bed8fb062f2676"): 47_900_592}
+MEASURED_TRAFFIC = {("single-seq-looped-bf16", "eee63ebbb572754b"): 47_900_635}
 TRAFFIC_SOURCES = ["paper_2609_34538_amd/csrc/attn_mfma.hip",
                    "paper_2609_34538_amd/csrc/attn_combine.hip",
                    "paper_2609_34538_amd/csrc/das_api.hip",

@@ -242,7 +242,8 @@ das_status das_attn_policy(const das_cache *cache, const das_batch *batch,
  *
  * The target pages must already be present in block_table. The verifier's
  * block K/V at plane p and layer l, k_new[p][l], is the same buffer the
- * attention calls take as k_blk.
+ * attention calls take as k_blk. DAS_ERR_SHAPE when w_max is outside
+ * 1..DAS_MAX_BLOCK or planes x L x Hkv exceeds 2^28.
  */
 das_status das_kv_append(const das_cache *cache, const das_batch *batch,
                          const void *k_new, const void *v_new, int32_t w_max,

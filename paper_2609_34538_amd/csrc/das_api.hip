@@ -259,6 +259,12 @@ das_status das_kv_append(const das_cache *cache, const das_batch *batch, const v
       !aligned(len_out, 4))
     return DAS_ERR_ALIGN;
   if (w_max < 1 || w_max > DAS_MAX_BLOCK) return DAS_ERR_SHAPE;
+  // (plane, layer, KV head) work units and the grid stay within int32
+  const long units = static_cast<long>(cache->num_k_planes > cache->num_v_planes
+                                           ? cache->num_k_planes
+                                           : cache->num_v_planes) *
+                     cache->num_layers * cache->num_kv_heads;
+  if (units > (1L << 28)) return DAS_ERR_SHAPE;
   if (len_out && static_cast<const void *>(len_out) ==
                      static_cast<const void *>(batch->prefix_len))
     return DAS_ERR_SHAPE;

@@ -210,6 +210,9 @@ def test_append_argument_checks():
     bad = make_cache()
     bad.head_dim = 100
     assert app(cc=bad) == SHAPE
+    big = make_cache()
+    big.num_layers = 1 << 26  # 2 key planes x 2^26 layers x 8 heads: past 2^28 work units
+    assert app(cc=big) == SHAPE
     nb = make_batch()
     nb.block_table = None
     assert app(bb=nb) == NULL
