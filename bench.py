@@ -1,25 +1,29 @@
 """Benchmark of the DAS hot path on one MI355X.
 
 A step is one pass of the whole hot path over one batch of synthetic input:
-the Mature-V draft attention of every core layer (keys at the draft depth d,
-values at the full depth R), the full-depth verifier attention of every core
-layer over the same block, and the commit of the accepted block K/V into the
-depth-indexed paged cache. Inputs are resident in HBM before timing starts.
+the draft attention stacks of the workload (each stack = the L core-layer
+calls of one recurrent application: Mature-V reads, keys at the draft depth
+d, values at the full depth R), the full-depth verifier stack over the final
+block, and the commit of the accepted block K/V into the depth-indexed paged
+cache. Inputs are resident in HBM before timing starts.
 
-Default workload: a single sequence shaped like the paper's looped models
-(bf16, 55 query = 55 KV heads, head_dim 96, verified prefix 2048, draft block
-8, R = 32, d = 4, 4 core layers, every depth of the cache stored).
-Successive steps rotate over disjoint copies of the cache pages so that the
-bytes a step reads are not served by the 256 MB last-level cache. Each step
-is captured once per cache copy as a HIP graph and replayed (--eager launches
-every call from the host instead).
+Default workload: the DAS-Wave step (bf16, batch 32, verified prefixes
+uniform in [4096, 8192], 55 query = 55 KV heads, head_dim 96, R = 32, 4 core
+layers; draft rounds at depths 1..4 over blocks of 4, 8, 16 and 32 tokens,
+the verifier at depth 32 over 32 tokens, the commit of U{0..32} accepted
+tokens per sequence). Cache copies rotate per stack, so the same prefix
+bytes are read again only after at least 1 GB of other reads, past the
+256 MB last-level cache. Each step is captured as a HIP graph and replayed
+(--eager launches every call from the host instead).
 
-Prints one JSON line: throughput (block tokens per second, HIP events around
-the timed steps), the roofline of the dominant kernel (the attention launch =
-attention kernel + split combine, HBM bound: algorithmic bytes over the
-average launch duration, from HIP events around replays of each step's
-attention launches on the same stream right after the timed steps), and the
-fp64 oracle timed on the host's cores on a bounded sample.
+Prints one JSON line: throughput (block tokens verified per second, HIP
+events around the timed steps; per-step median, p10, p90), per-stack tokens/s
+(B * w over one stack's calls, median, p10, p90), the roofline of the dominant
+kernel (the attention launch = attention kernel + split combine, HBM bound:
+algorithmic bytes over the average launch duration, from HIP events around
+replays of each step's attention launches on the same stream right after the
+timed steps), the host CPU model, and the fp64 oracle timed on the host's
+cores on a bounded sample.
 """
 
 from __future__ import annotations
@@ -62,9 +66,9 @@ def kernel_digest():
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--config", type=int, default=2, help="workload index (1-5)")
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=5, help="workload index (1-5)")
     ap.add_argument("--path", default="auto", choices=["auto", "valu", "mfma"])
     ap.add_argument("--pps", type=int, default=0, help="prefix pages per split (0 = library)")
     ap.add_argument("--rotate-bytes", type=float, default=1.0e9,
@@ -105,13 +109,15 @@ def algorithmic_append_bytes(wl, nk, nv, num_new):
     return 2 * int(np.sum(num_new)) * (nk + nv) * wl.layers * wl.hkv * wl.dh * e
 
 
-def cpu_baseline(cd, calls, seconds, tokens_per_step, max_seqs=4, max_reads=8):
+def cpu_baseline(cd, calls, seconds, tokens_per_step, max_seqs=4, max_reads=8,
+                 max_prefix_bytes=4.0e9):
     """Time the fp64 oracle on a bounded sample of the step's attention calls
     and scale it to a whole step: per block width, calls are cycled over at
-    most `max_reads` distinct (layer, kappa, nu) prefix reads and the first
-    `max_seqs` sequences for that width's share of the time budget; the mean
-    time per call is scaled by sum(S_b + w) of the batch over that of the
-    sample (the oracle's work is linear in it) and summed over the step."""
+    most `max_reads` distinct (layer, kappa, nu) prefix reads (fewer when the
+    fp64 copies of the sampled prefixes would exceed `max_prefix_bytes`) and
+    the first `max_seqs` sequences for that width's share of the time budget;
+    the mean time per call is scaled by sum(S_b + w) of the batch over that of
+    the sample (the oracle's work is linear in it) and summed over the step."""
     import torch
     from oracle import das_oracle as orc
     from paper_2609_34538_amd import datagen as dg
@@ -124,29 +130,37 @@ def cpu_baseline(cd, calls, seconds, tokens_per_step, max_seqs=4, max_reads=8):
     by_w = {}
     for c in calls:
         by_w.setdefault(int(c[3].shape[1]), []).append(c)
-    prefix, blocks = {}, {}
+    # fp64 prefix K and V of one (layer, kappa, nu) read over the sampled sequences
+    read_bytes = 2 * float(np.sum(lens[seqs])) * wl.hkv * wl.dh * 8
+    max_reads = max(1, min(max_reads, int(max_prefix_bytes // max(read_bytes, 1))))
 
-    def args_of(c, b):
-        layer, kappa, nu, q, kb, vb = c
-        key = (b, layer, kappa, nu)
-        if key not in prefix:
-            s_len = int(cd.prefix_lens[b])
-            prefix[key] = (dg.gather_prefix_k(cd, b, cd.k_plane[kappa], layer, s_len),
-                           dg.gather_prefix_v(cd, b, cd.v_plane[nu], layer, s_len))
-        bkey = (b, q.data_ptr(), kb.data_ptr(), vb.data_ptr())
-        if bkey not in blocks:
-            blocks[bkey] = tuple(t[b].double().cpu().numpy() for t in (q, kb, vb))
-        qb, kbb, vbb = blocks[bkey]
-        return qb, prefix[key][0], prefix[key][1], kbb, vbb
-
-    t_call, done_total = {}, 0
+    t_call, done_total, n_reads = {}, 0, 0
     for w, cl in by_w.items():
+        prefix, blocks = {}, {}
+
+        def args_of(c, b):
+            layer, kappa, nu, q, kb, vb = c
+            key = (b, layer, kappa, nu)
+            if key not in prefix:
+                s_len = int(cd.prefix_lens[b])
+                prefix[key] = (dg.gather_prefix_k(cd, b, cd.k_plane[kappa], layer, s_len),
+                               dg.gather_prefix_v(cd, b, cd.v_plane[nu], layer, s_len))
+            bkey = (b, q.data_ptr(), kb.data_ptr(), vb.data_ptr())
+            if bkey not in blocks:
+                blocks[bkey] = tuple(t[b].double().cpu().numpy() for t in (q, kb, vb))
+            qb, kbb, vbb = blocks[bkey]
+            return qb, prefix[key][0], prefix[key][1], kbb, vbb
+
         reads = []
         for c in cl:
             if (c[0], c[1], c[2]) not in reads and len(reads) < max_reads:
                 reads.append((c[0], c[1], c[2]))
+        n_reads = max(n_reads, len(reads))
         sample = [c for c in cl if (c[0], c[1], c[2]) in reads]
         budget = seconds * len(cl) / len(calls)
+        for b in seqs:  # gather the sample's inputs before the clock starts
+            for c in sample:
+                args_of(c, b)
         done = 0
         t0 = time.perf_counter()
         while True:
@@ -160,14 +174,57 @@ def cpu_baseline(cd, calls, seconds, tokens_per_step, max_seqs=4, max_reads=8):
         scale = float(np.sum(lens + w) / np.sum(lens[seqs] + w))
         t_call[w] = el / done * scale
         done_total += done
+        del prefix, blocks
     step_s = sum(t_call[int(c[3].shape[1])] for c in calls)
     return {"value": tokens_per_step / step_s, "unit": "tokens/s", "cores": cores,
             "kind": "oracle",
-            "sample": (f"{done_total} fp64 oracle calls (each over {len(seqs)} of {wl.batch} "
-                       f"sequences; {sum(len(v) for v in by_w.values())} attention calls per "
-                       f"step, block widths {sorted(by_w)}) in about {seconds:.0f} s, scaled by "
-                       f"prefix length to the batch and summed over the step's calls; commit "
-                       f"not included")}
+            "sample": (f"{done_total} fp64 oracle calls, each over {len(seqs)} of {wl.batch} "
+                       f"sequences, cycling over at most {n_reads} (layer, kappa, nu) prefix "
+                       f"reads per block width ({len(calls)} attention calls per step, widths "
+                       f"{sorted(by_w)}), about {seconds:.0f} s in all; the mean time per call "
+                       f"is scaled by prefix length to the batch and summed over the step's "
+                       f"calls; commit not included")}
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
+def pct(xs, p):
+    return float(np.percentile(np.asarray(xs, dtype=np.float64), p))
+
+
+def build_stacks(args, wl):
+    """The attention stacks of one step, in issue order. A stack is the L
+    core-layer calls of one recurrent application (one draft round, or the
+    verifier at one depth): (kind, width, block depth, [(layer, kappa, nu)])."""
+    R, L = wl.depth_R, wl.layers
+    stacks = []
+    if args.draft == "wave":
+        J, gamma, w_init = 24, 32, 2
+        for j in range(J):
+            w = min(gamma, w_init + j)  # Eq. (5)
+            for _ in range(args.wave_k):
+                stacks.append(("draft", w, R, [(layer, R, R) for layer in range(L)]))
+        wv = min(32, w_init + J)  # the anchor and the schedule's final proposals
+    else:
+        pol = {"maturev": lambda d: (d, R), "deepkv": lambda d: (R, R),
+               "deepk": lambda d: (R, d), "aligned": lambda d: (d, d)}[args.draft_policy]
+        for d, w in zip(wl.draft_depths, wl.draft_widths):
+            stacks.append(("draft", w, d, [(layer,) + pol(d) for layer in range(L)]))
+        wv = wl.verify_width
+    vdepths = [R] if args.verify == "single" else list(range(1, R + 1))
+    for r in vdepths:
+        stacks.append(("verify", wv, r, [(layer, r, r) for layer in range(L)]))
+    return stacks, wv, vdepths
 
 
 def main():
@@ -191,52 +248,24 @@ def main():
 
     dev = "cuda"
     wl = dg.WORKLOADS[args.config]
-    R, L, wv = wl.depth_R, wl.layers, wl.verify_width
-    if args.draft == "wave":
-        # the verifier consumes the anchor and the schedule's final proposals
-        wv = min(32, 2 + 24)
-    # The calls of one step: (kind, layer, kappa, nu, width, block depth,
-    # rotation group). Calls of rotation group g on the step's cache copy c read copy
-    # (c + g) mod copies, so repeated reads of the same prefix bytes inside a
-    # step are also >= rotate_bytes apart.
-    plan = []
-    if args.draft == "wave":
-        J, gamma, w_init = 24, 32, 2
-        widths = [min(gamma, w_init + j) for j in range(J)]  # Eq. (5)
-        for j, w in enumerate(widths):
-            for _ in range(args.wave_k):
-                for layer in range(L):
-                    plan.append(("draft", layer, R, R, w, R, j))
-        n_groups = J
-    else:
-        pol = {"maturev": lambda d: (d, R), "deepkv": lambda d: (R, R),
-               "deepk": lambda d: (R, d), "aligned": lambda d: (d, d)}[args.draft_policy]
-        for layer in range(L):
-            for d, w in zip(wl.draft_depths, wl.draft_widths):
-                kappa, nu = pol(d)
-                plan.append(("draft", layer, kappa, nu, w, d, 0))
-        n_groups = 1
-    vdepths = [R] if args.verify == "single" else list(range(1, R + 1))
-    for r in vdepths:
-        for layer in range(L):
-            plan.append(("verify", layer, r, r, wv, r, 0))
+    R = wl.depth_R
+    stacks, wv, vdepths = build_stacks(args, wl)
     kd, vd = set(wl.k_depths()), set(wl.v_depths())
-    missing = sorted({e[2] for e in plan} - kd) + sorted({e[3] for e in plan} - vd)
+    missing = (sorted({c[1] for s in stacks for c in s[3]} - kd)
+               + sorted({c[2] for s in stacks for c in s[3]} - vd))
     if missing:
         print(json.dumps({"error": f"depths {missing} are not stored in workload {wl.name}"}))
         sys.exit(2)
 
-    # bytes one step reads (and bytes between reuses of one rotation group), to
-    # size the cache rotation
+    # Cache rotation: stack j of step i reads copy (i * n_stacks + j) mod copies,
+    # so the same prefix bytes (the value plane is read by every stack) are read
+    # again only after `copies` whole stacks, at least rotate_bytes later.
     rng_lens = np.random.default_rng(wl.seed).integers(wl.prefix[0], wl.prefix[1] + 1,
                                                        size=wl.batch)
-    step_read = sum(algorithmic_attn_bytes(wl, rng_lens, e[4]) for e in plan)
-    if n_groups > 1:
-        group_read = step_read / n_groups
-        copies = 1 + math.ceil(args.rotate_bytes / max(group_read, 1))
-    else:
-        copies = math.ceil(args.rotate_bytes / max(step_read, 1))
-    copies = max(1, min(16, copies))
+    stack_read = min(algorithmic_attn_bytes(wl, rng_lens, s[1]) * len(s[3]) for s in stacks)
+    copies = max(1, min(16, math.ceil(args.rotate_bytes / max(stack_read, 1))))
+    n_stacks = len(stacks)
+    period = copies // math.gcd(copies, n_stacks)  # steps until the copy pattern repeats
     cd = dg.make_cache(wl, dev, copies=copies, spare_tokens=max(wl.w_max, wv))
     lens = cd.prefix_lens
     cache = das.PagedCache(cd.k_pool, cd.v_pool, R, cd.k_plane, cd.v_plane)
@@ -247,12 +276,12 @@ def main():
     k_new, v_new, num_new = dg.commit_inputs(cd, wv, dev)
     num_new_t = torch.as_tensor(num_new, device=dev)
     block_in, outs = {}, {}
-    for _, layer, kappa, nu, w, depth, _ in plan:
+    for _, w, depth, _ in stacks:
         if (w, depth) not in block_in:
             block_in[(w, depth)] = dg.block_inputs(cd, w, depth, dev)
             outs[(w, depth)] = torch.empty_like(block_in[(w, depth)][0])
     opts = dict(path=args.path, pages_per_split=args.pps)
-    wmax = max(e[4] for e in plan)
+    wmax = max(s[1] for s in stacks)
     ws = das.alloc_workspace(cache, batches[0], wl.hq, wmax, **opts)
     len_out = torch.empty(wl.batch, dtype=torch.int32, device=dev)
     if args.accept:
@@ -263,8 +292,8 @@ def main():
     else:
         commit_count_t = num_new_t
     # A stream of its own (default priority): graphs cannot be captured on
-    # the legacy default stream.
-    # Graph replays launch on the current stream, so it is made current.
+    # the legacy default stream. Graph replays launch on the current stream,
+    # so it is made current.
     stream = torch.cuda.Stream()
     torch.cuda.synchronize()
     torch.cuda.set_stream(stream)
@@ -276,104 +305,116 @@ def main():
             kb, vb = k_new[cd.k_plane[depth], layer], v_new[cd.v_plane[depth], layer]
         return q, kb, vb, outs[(w, depth)]
 
-    # Every call of a step, marshalled once per starting cache copy.
-    step_calls = []
-    for c in range(copies):
-        seq = []
-        for kind, layer, kappa, nu, w, depth, g in plan:
-            q, kb, vb, out = attn_args(kind, layer, w, depth)
-            seq.append((w, das.PreparedAttention(cache, batches[(c + g) % copies], layer, kappa,
-                                                 nu, q, kb, vb, out, ws, stream=stream, **opts)))
+    # Every call of a step, marshalled once per step of the rotation period:
+    # per stack a list of prepared attention calls, then the tail (acceptance
+    # and commit).
+    step_stacks, step_tail = [], []
+    for i in range(period):
+        per = []
+        for j, (kind, w, depth, calls) in enumerate(stacks):
+            copy = (i * n_stacks + j) % copies
+            per.append([das.PreparedAttention(cache, batches[copy], layer, kappa, nu,
+                                              *attn_args(kind, layer, w, depth), ws,
+                                              stream=stream, **opts)
+                        for layer, kappa, nu in calls])
+        tail = []
         if args.accept:
-            seq.append((None, lambda: das.greedy_accept(y_t, yhat_t, m_t, accepted=acc_t,
-                                                        num_keep=keep_t, stream=stream)))
+            tail.append(lambda: das.greedy_accept(y_t, yhat_t, m_t, accepted=acc_t,
+                                                  num_keep=keep_t, stream=stream))
         if not args.attn_only:
-            seq.append((None, das.PreparedAppend(cache, batches[c], k_new, v_new, commit_count_t,
-                                                 len_out, stream=stream)))
-        step_calls.append(seq)
-    n_attn = sum(1 for w, _ in step_calls[0] if w is not None)
-    widths = [w for w, _ in step_calls[0] if w is not None]
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(args.steps if not args.eager else n_attn * args.steps)]
-    spans = []  # (start event, end event, attention launches covered)
+            last = ((i + 1) * n_stacks - 1) % copies  # the verifier's copy
+            tail.append(das.PreparedAppend(cache, batches[last], k_new, v_new, commit_count_t,
+                                           len_out, stream=stream))
+        step_stacks.append(per)
+        step_tail.append(tail)
+    n_attn = sum(len(s[3]) for s in stacks)
+
+    def run_step(i):
+        for st in step_stacks[i % period]:
+            for call in st:
+                call()
+        for call in step_tail[i % period]:
+            call()
+
+    def run_attn(i):
+        for st in step_stacks[i % period]:
+            for call in st:
+                call()
+
+    def run_stack(i, j):
+        for call in step_stacks[i % period][j]:
+            call()
 
     if args.eager:
-        def step(i, timed):
-            k = 0
-            for w, call in step_calls[i % copies]:
-                if timed and w is not None:
-                    e0, e1 = ev[(i * n_attn) + k]
-                    e0.record(stream)
-                    call()
-                    e1.record(stream)
-                    spans.append((e0, e1, [w]))
-                    k += 1
-                else:
-                    call()
+        step_fn, attn_fn, stack_fn = run_step, run_attn, run_stack
     else:
-        # Per cache copy: one graph holding the whole step (every attention
-        # launch, then the commit), replayed for the timed steps, and one
-        # holding only the step's attention launches, replayed between HIP
-        # events afterwards to time the attention launches on their own.
-        for seq in step_calls:  # eager pass first: per-device state is set up
-            for _, call in seq:
-                call()
-        torch.cuda.synchronize()
-        graphs = []
-        for seq in step_calls:
-            g_step = torch.cuda.CUDAGraph()
-            with torch.cuda.graph(g_step, stream=stream):
-                for w, call in seq:
-                    if w is not None:
-                        call()
-                for w, call in seq:
-                    if w is None:
-                        call()
-            g_attn = torch.cuda.CUDAGraph()
-            with torch.cuda.graph(g_attn, stream=stream):
-                for w, call in seq:
-                    if w is not None:
-                        call()
-            graphs.append((g_step, g_attn))
+        # Per step of the rotation period: one graph holding the whole step,
+        # one holding only its attention launches and one per stack, each
+        # replayed between HIP events (events cannot sit inside a graph).
+        for i in range(period):  # eager pass first: per-device state is set up
+            run_step(i)
         torch.cuda.synchronize()
 
-        def step(i, timed):
-            graphs[i % copies][0].replay()
+        def capture(fn):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=stream):
+                fn()
+            return g
 
-    for i in range(args.warmup):
-        step(i, False)
-    torch.cuda.synchronize()
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
-    t_start.record(stream)
-    for i in range(args.steps):
-        step(i, True)
-    t_end.record(stream)
-    torch.cuda.synchronize()
-    total_ms = t_start.elapsed_time(t_end)
+        g_step = [capture(lambda i=i: run_step(i)) for i in range(period)]
+        g_attn = [capture(lambda i=i: run_attn(i)) for i in range(period)]
+        g_stack = [[capture(lambda i=i, j=j: run_stack(i, j)) for j in range(n_stacks)]
+                   for i in range(period)]
+        torch.cuda.synchronize()
+        step_fn = lambda i: g_step[i % period].replay()  # noqa: E731
+        attn_fn = lambda i: g_attn[i % period].replay()  # noqa: E731
+        stack_fn = lambda i, j: g_stack[i % period][j].replay()  # noqa: E731
+
+    def timed(fn, n, warm):
+        """Durations (ms) of fn(i), i < n, between HIP events on the stream."""
+        for i in range(warm):
+            fn(i)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+        ev[0].record(stream)
+        for i in range(n):
+            fn(i)
+            ev[i + 1].record(stream)
+        torch.cuda.synchronize()
+        return [ev[i].elapsed_time(ev[i + 1]) for i in range(n)], ev[0].elapsed_time(ev[n])
+
+    # the timed steps
+    step_ms, total_ms = timed(step_fn, args.steps, args.warmup)
     ms_step = total_ms / args.steps
     tokens_per_step = wl.batch * wv  # block tokens verified per step
     value = tokens_per_step / (ms_step / 1e3)
 
-    if not args.eager:
-        # attention launches alone: the same steps' attention graphs between events
-        for i in range(args.warmup):
-            graphs[i % copies][1].replay()
-        for i in range(args.steps):
-            e0, e1 = ev[i]
-            e0.record(stream)
-            graphs[i % copies][1].replay()
-            e1.record(stream)
-            spans.append((e0, e1, widths))
-        torch.cuda.synchronize()
-
-    # dominant kernel: the attention launches
-    attn_total_ms = sum(a.elapsed_time(b) for a, b, _ in spans)
-    launches = [w for _, _, ws_ in spans for w in ws_]
-    attn_ms = attn_total_ms / len(launches)
-    bytes_per = float(np.mean([algorithmic_attn_bytes(wl, lens, w) for w in launches]))
+    # dominant kernel: the attention launches (attention kernel + split merge),
+    # replayed without the commit between events after the timed steps
+    attn_ms_steps, _ = timed(attn_fn, args.steps, min(args.warmup, 3))
+    attn_ms = float(np.mean(attn_ms_steps)) / n_attn
+    launch_bytes = [algorithmic_attn_bytes(wl, lens, s[1]) for s in stacks for _ in s[3]]
+    bytes_per = float(np.mean(launch_bytes))
     achieved = bytes_per / (attn_ms / 1e3) / 1e9
-    step_bytes = (sum(algorithmic_attn_bytes(wl, lens, e[4]) for e in plan)
+
+    # per-stack tokens/s (B * w over the L core-layer calls of one stack)
+    stack_rows = []
+    for j, (kind, w, depth, calls) in enumerate(stacks):
+        ms, _ = timed(lambda i, j=j: stack_fn(i, j), args.steps, 1)
+        by = algorithmic_attn_bytes(wl, lens, w) * len(calls)
+        med = pct(ms, 50)
+        stack_rows.append({
+            "kind": kind, "width": w, "kappa": calls[0][1], "nu": calls[0][2],
+            "calls": len(calls),
+            "ms": {"median": med, "p10": pct(ms, 10), "p90": pct(ms, 90)},
+            "tokens_per_s": {"median": wl.batch * w / (med / 1e3),
+                             "p10": wl.batch * w / (pct(ms, 90) / 1e3),
+                             "p90": wl.batch * w / (pct(ms, 10) / 1e3)},
+            "hbm_frac_median": by / (med / 1e3) / 1e9 / HBM_PEAK_GBS})
+    if len(stack_rows) > 8:  # the schedule's rounds: keep the ends and the verifier
+        keep = stack_rows[:2] + stack_rows[-3:]
+        stack_rows = keep
+
+    step_bytes = (sum(algorithmic_attn_bytes(wl, lens, s[1]) * len(s[3]) for s in stacks)
                   + (0 if args.attn_only else
                      algorithmic_append_bytes(wl, cd.k_pool.shape[0], cd.v_pool.shape[0],
                                               num_new)))
@@ -381,6 +422,10 @@ def main():
     default_plan = (args.path == "auto" and args.pps == 0 and args.draft == "workload"
                     and args.draft_policy == "maturev" and args.verify == "single")
     traffic = MEASURED_TRAFFIC.get((wl.name, kernel_digest())) if default_plan else None
+    timing = ("HIP events around each step's attention launches"
+              if args.eager else
+              "HIP events around replays of each step's attention launches (one graph per "
+              "step), run after the timed steps on the same stream")
     result = {
         "metric": "Mature-V draft-block attention tokens/s + achieved HBM GB/s (% of 8 TB/s)",
         "value": value,
@@ -399,29 +444,32 @@ def main():
                                                                           int(lens.max())],
                    "draft": (f"das-wave J=24 gamma=32 W_init=2 k={args.wave_k}"
                              if args.draft == "wave" else "workload rounds"),
-                   "draft_calls": sorted({(e[2], e[3], e[4]) for e in plan if e[0] == "draft"}),
+                   "draft_calls": sorted({(c[1], c[2], s[1]) for s in stacks
+                                          if s[0] == "draft" for c in s[3]}),
                    "verify": {"depths": [vdepths[0], vdepths[-1]], "width": wv},
                    "depth_R": R, "accept_on_device": args.accept,
                    "core_layers": wl.layers, "path": args.path,
                    "pages_per_split": args.pps, "cache_copies_rotated": copies,
                    "launch": "eager" if args.eager else "hip_graph",
                    "commit": not args.attn_only},
+        "step_ms": {"median": pct(step_ms, 50), "p10": pct(step_ms, 10),
+                    "p90": pct(step_ms, 90)},
         "step_hbm_gbs": step_bytes / (ms_step / 1e3) / 1e9,
         "step_frac_of_8tbs": step_bytes / (ms_step / 1e3) / 1e9 / HBM_PEAK_GBS,
+        "stacks": stack_rows,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
                      "kernel": "attention launch (partial + split combine)",
-                     "timing": ("HIP events around each attention launch in the timed steps"
-                                if args.eager else
-                                "HIP events around replays of each step's attention launches, "
-                                "run after the timed steps on the same stream"),
-                     "avg_launch_us": attn_ms * 1e3, "bytes_per_launch": bytes_per},
+                     "timing": timing, "avg_launch_us": attn_ms * 1e3,
+                     "bytes_per_launch": bytes_per},
+        "host_cpu": cpu_model(),
     }
     if not args.no_cpu:
         calls = []
-        for kind, layer, kappa, nu, w, depth, _ in plan:
-            q, kb, vb, _ = attn_args(kind, layer, w, depth)
-            calls.append((layer, kappa, nu, q, kb, vb))
+        for kind, w, depth, cl in stacks:
+            for layer, kappa, nu in cl:
+                q, kb, vb, _ = attn_args(kind, layer, w, depth)
+                calls.append((layer, kappa, nu, q, kb, vb))
         result["cpu_baseline"] = cpu_baseline(cd, calls, args.cpu_seconds, tokens_per_step)
     print(json.dumps(result))
 

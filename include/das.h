@@ -27,8 +27,12 @@
  *   the caller's next synchronisation of that stream.
  * - Errors: every argument check runs on the host before any HIP call. A
  *   failed check returns a negative das_status and enqueues nothing. A
- *   failed kernel launch returns DAS_ERR_HIP. No exception and no exit()
- *   crosses this boundary.
+ *   failed kernel launch returns DAS_ERR_HIP; the status is that of the
+ *   library's own launches, so an error left pending by the caller's earlier
+ *   HIP work is neither reported as the library's nor cleared. Requests whose
+ *   launch grid would exceed what HIP accepts (2^32 - 1 work-items along a
+ *   grid dimension) are rejected with DAS_ERR_SHAPE. No exception and no
+ *   exit() crosses this boundary.
  * - Device-side range checks: when `dev_error` in das_batch is non-NULL the
  *   kernels OR bits into it (DAS_DEVERR_*) for out-of-range page ids,
  *   prefix lengths or commit counts, and skip the offending data instead of
@@ -114,7 +118,7 @@ typedef struct das_cache {
   int32_t dtype;         /* das_dtype of every K/V/Q/O element               */
   int32_t num_depths;    /* R, 1..DAS_MAX_DEPTH                              */
   int32_t num_layers;    /* L core layers, >= 1                              */
-  int32_t num_kv_heads;  /* Hkv, >= 1                                        */
+  int32_t num_kv_heads;  /* Hkv, 1..65535                                    */
   int32_t head_dim;      /* 64, 96 or 128                                    */
   int32_t num_pages;     /* physical pages per (plane, layer, head), >= 1    */
   int32_t num_k_planes;  /* >= 1                                             */
@@ -243,7 +247,8 @@ das_status das_attn_policy(const das_cache *cache, const das_batch *batch,
  * The target pages must already be present in block_table. The verifier's
  * block K/V at plane p and layer l, k_new[p][l], is the same buffer the
  * attention calls take as k_blk. DAS_ERR_SHAPE when w_max is outside
- * 1..DAS_MAX_BLOCK or planes x L x Hkv exceeds 2^28.
+ * 1..DAS_MAX_BLOCK or the commit's grid (one 64-lane wave per (plane, layer,
+ * KV head), four per workgroup) exceeds 2^32 - 1 work-items.
  */
 das_status das_kv_append(const das_cache *cache, const das_batch *batch,
                          const void *k_new, const void *v_new, int32_t w_max,

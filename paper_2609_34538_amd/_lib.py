@@ -244,6 +244,21 @@ def _check_block(cache: PagedCache, batch: Batch, q, k_blk, v_blk):
     return w, hq
 
 
+def _check_outputs(cache: PagedCache, batch: Batch, q, out, lse):
+    """out: same shape, dtype and device as q, contiguous; lse: contiguous
+    fp32 [B, Hq, w] on the cache's device."""
+    if out is not None:
+        if (out.shape != q.shape or out.dtype != q.dtype or not out.is_contiguous()
+                or out.device != cache.k_pool.device):
+            raise ValueError("out must be a contiguous tensor shaped and typed like q")
+    if lse is not None:
+        B, w, hq, _ = q.shape
+        if (lse.dtype != torch.float32 or tuple(lse.shape) != (B, hq, w)
+                or not lse.is_contiguous() or lse.device != cache.k_pool.device):
+            raise ValueError("lse must be a contiguous float32 tensor [B, Hq, w] on the "
+                             "cache's device")
+
+
 def attn_policy(cache: PagedCache, batch: Batch, layer: int, kappa: int, nu: int,
                 q: torch.Tensor, k_blk: torch.Tensor, v_blk: torch.Tensor,
                 out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
@@ -251,6 +266,7 @@ def attn_policy(cache: PagedCache, batch: Batch, layer: int, kappa: int, nu: int
                 pages_per_split: int = 0, stream=None) -> torch.Tensor:
     """Eq. (2)-(3) with prefix keys at depth kappa and values at depth nu."""
     w, hq = _check_block(cache, batch, q, k_blk, v_blk)
+    _check_outputs(cache, batch, q, out, lse)
     if out is None:
         out = torch.empty_like(q)
     if workspace is None:
@@ -275,8 +291,7 @@ class PreparedAttention:
                  out: torch.Tensor, workspace: torch.Tensor, lse: Optional[torch.Tensor] = None,
                  path: str = "auto", pages_per_split: int = 0, stream=None):
         w, hq = _check_block(cache, batch, q, k_blk, v_blk)
-        if out.shape != q.shape or out.dtype != q.dtype or not out.is_contiguous():
-            raise ValueError("out must match q")
+        _check_outputs(cache, batch, q, out, lse)
         self._keep = (cache, batch, q, k_blk, v_blk, out, workspace, lse)
         self._opts = _options(path, pages_per_split)
         self._fn = LIB.das_attn_policy
@@ -296,12 +311,11 @@ class PreparedAppend:
 
     def __init__(self, cache: PagedCache, batch: Batch, k_new: torch.Tensor, v_new: torch.Tensor,
                  num_new: torch.Tensor, len_out: Optional[torch.Tensor] = None, stream=None):
-        if k_new.dim() != 6 or num_new.dtype != torch.int32:
-            raise ValueError("k_new must be 6-d and num_new int32")
+        w_max = _check_append(cache, batch, k_new, v_new, num_new, len_out)
         self._keep = (cache, batch, k_new, v_new, num_new, len_out)
         self._fn = LIB.das_kv_append
         self._args = (ctypes.byref(cache.c), ctypes.byref(batch.c), k_new.data_ptr(),
-                      v_new.data_ptr(), k_new.shape[3], num_new.data_ptr(), _ptr(len_out),
+                      v_new.data_ptr(), w_max, num_new.data_ptr(), _ptr(len_out),
                       _stream_handle(stream))
 
     def __call__(self):
@@ -314,6 +328,7 @@ def attn_draft_maturev(cache: PagedCache, batch: Batch, layer: int, draft_depth:
                        q, k_blk, v_blk, out=None, lse=None, workspace=None, stream=None):
     """Mature-V draft read: keys at draft_depth, values at the full depth R."""
     w, hq = _check_block(cache, batch, q, k_blk, v_blk)
+    _check_outputs(cache, batch, q, out, lse)
     if out is None:
         out = torch.empty_like(q)
     if workspace is None:
@@ -332,6 +347,7 @@ def attn_verify(cache: PagedCache, batch: Batch, layer: int, depth: int, q, k_bl
                 out=None, lse=None, workspace=None, stream=None):
     """The target's aligned read at `depth` (the full-depth verifier at R)."""
     w, hq = _check_block(cache, batch, q, k_blk, v_blk)
+    _check_outputs(cache, batch, q, out, lse)
     if out is None:
         out = torch.empty_like(q)
     if workspace is None:
@@ -345,9 +361,10 @@ def attn_verify(cache: PagedCache, batch: Batch, layer: int, depth: int, q, k_bl
     return out
 
 
-def kv_append(cache: PagedCache, batch: Batch, k_new: torch.Tensor, v_new: torch.Tensor,
-              num_new: torch.Tensor, len_out: Optional[torch.Tensor] = None, stream=None):
-    """Commit the first num_new[b] block entries of every plane and layer."""
+def _check_append(cache: PagedCache, batch: Batch, k_new, v_new, num_new, len_out) -> int:
+    """Shapes of a commit's tensors; returns w_max."""
+    if k_new.dim() != 6:
+        raise ValueError("k_new must be [nK, L, B, w_max, Hkv, dh]")
     nk, L, B, w_max, hkv, dh = k_new.shape
     if (nk, L, B, hkv, dh) != (cache.k_pool.shape[0], cache.num_layers, batch.batch,
                                cache.num_kv_heads, cache.head_dim):
@@ -355,10 +372,21 @@ def kv_append(cache: PagedCache, batch: Batch, k_new: torch.Tensor, v_new: torch
     if tuple(v_new.shape) != (cache.v_pool.shape[0], L, B, w_max, hkv, dh):
         raise ValueError("v_new must be [nV, L, B, w_max, Hkv, dh]")
     for t in (k_new, v_new):
-        if t.dtype != cache.dtype or not t.is_contiguous():
-            raise ValueError("k_new / v_new must be contiguous in the cache dtype")
-    if num_new.dtype != torch.int32 or num_new.shape != (B,):
-        raise ValueError("num_new must be int32 [B]")
+        if (t.dtype != cache.dtype or not t.is_contiguous()
+                or t.device != cache.k_pool.device):
+            raise ValueError("k_new / v_new must be contiguous in the cache dtype and device")
+    if num_new.dtype != torch.int32 or tuple(num_new.shape) != (B,) or not num_new.is_contiguous():
+        raise ValueError("num_new must be a contiguous int32 tensor [B]")
+    if len_out is not None and (len_out.dtype != torch.int32 or tuple(len_out.shape) != (B,)
+                                or not len_out.is_contiguous()):
+        raise ValueError("len_out must be a contiguous int32 tensor [B]")
+    return w_max
+
+
+def kv_append(cache: PagedCache, batch: Batch, k_new: torch.Tensor, v_new: torch.Tensor,
+              num_new: torch.Tensor, len_out: Optional[torch.Tensor] = None, stream=None):
+    """Commit the first num_new[b] block entries of every plane and layer."""
+    w_max = _check_append(cache, batch, k_new, v_new, num_new, len_out)
     st = LIB.das_kv_append(ctypes.byref(cache.c), ctypes.byref(batch.c), k_new.data_ptr(),
                            v_new.data_ptr(), w_max, num_new.data_ptr(), _ptr(len_out),
                            _stream_handle(stream))

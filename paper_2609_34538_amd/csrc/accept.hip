@@ -49,8 +49,7 @@ __global__ __launch_bounds__(64 * kSeqPerBlock) void greedy_accept_kernel(Accept
 
 hipError_t launch_greedy_accept(const AcceptParams &p, hipStream_t s) {
   const int blocks = (p.batch + kSeqPerBlock - 1) / kSeqPerBlock;
-  hipLaunchKernelGGL(greedy_accept_kernel, dim3(blocks), dim3(64 * kSeqPerBlock), 0, s, p);
-  return hipGetLastError();
+  return launch_kernel(greedy_accept_kernel, dim3(blocks), dim3(64 * kSeqPerBlock), s, p);
 }
 
 }  // namespace das

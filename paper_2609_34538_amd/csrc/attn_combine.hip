@@ -109,8 +109,7 @@ template <typename T, int DH>
 hipError_t launch_typed(const AttnParams &p, int skip_single, hipStream_t s) {
   dim3 grid(p.batch * p.hkv, (p.rows + kRowsPerBlock - 1) / kRowsPerBlock,
             (DH + kColsPerBlock - 1) / kColsPerBlock);
-  hipLaunchKernelGGL((attn_combine_kernel<T, DH>), grid, dim3(64), 0, s, p, skip_single);
-  return hipGetLastError();
+  return launch_kernel(attn_combine_kernel<T, DH>, grid, dim3(64), s, p, skip_single);
 }
 
 }  // namespace

@@ -582,7 +582,7 @@ void attn_mfma_kernel(AttnParams p, int n_rg, int n_chunks) {
       if (lg == 0) {
         const size_t mrow =
             ((static_cast<size_t>(b) * p.hkv + kvh) * p.rows + row) * p.nsplit_ml + split;
-        p.ws_m[mrow] = st.m[qt] == kNegInf ? 0.f : st.m[qt];
+        p.ws_m[mrow] = st.m[qt];  // -inf when no position was visible: weight 0 in the merge
         p.ws_l[mrow] = st.l[qt];
       }
     }
@@ -596,9 +596,8 @@ hipError_t launch_typed(const AttnParams &p, hipStream_t s) {
   // every possible chunk (the table width bounds the splits of a sequence)
   const long chunks = static_cast<long>(p.batch) * p.hkv * p.nsplit * n_rg;
   if (chunks > 0x7fffffffL) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((attn_mfma_kernel<DH, NQ, NB, NW>), dim3(static_cast<unsigned>(chunks)),
-                     dim3(64 * NW), 0, s, p, n_rg, static_cast<int>(chunks));
-  return hipGetLastError();
+  return launch_kernel(attn_mfma_kernel<DH, NQ, NB, NW>, dim3(static_cast<unsigned>(chunks)),
+                       dim3(64 * NW), s, p, n_rg, static_cast<int>(chunks));
 }
 
 // Up to 32 query rows: one wave per chunk. More rows (GQA blocks): the row
@@ -609,6 +608,9 @@ hipError_t launch_typed(const AttnParams &p, hipStream_t s) {
 // one would leave one wave per SIMD at head dim 128).
 template <int DH>
 hipError_t launch_dh(const AttnParams &p, hipStream_t s) {
+  static_assert(mfma_tiles_per_wave(16) == 1 && mfma_tiles_per_wave(17) == 2 &&
+                mfma_waves(32) == 1 && mfma_waves(64) == 2 && mfma_waves(65) == 4,
+                "host-side grid checks mirror these shapes");
   if (p.rows <= 16) return launch_typed<DH, 1, 2, 1>(p, s);
   if (p.rows <= 32) return launch_typed<DH, 2, 2, 1>(p, s);
   if (p.rows <= 64) return launch_typed<DH, 2, 2, 2>(p, s);

@@ -336,8 +336,7 @@ template <typename T, int DH, int RT>
 hipError_t launch_rt(const AttnParams &p, hipStream_t s) {
   const int n_rt = (p.rows + RT - 1) / RT;
   dim3 grid(p.nsplit, p.hkv, p.batch * n_rt);
-  hipLaunchKernelGGL((attn_valu_kernel<T, DH, RT>), grid, dim3(256), 0, s, p);
-  return hipGetLastError();
+  return launch_kernel(attn_valu_kernel<T, DH, RT>, grid, dim3(256), s, p);
 }
 
 template <typename T, int DH>

@@ -27,6 +27,7 @@ das_status check_cache(const das_cache *c) {
   if (c->dtype != DAS_F32 && c->dtype != DAS_BF16) return DAS_ERR_DTYPE;
   if (c->num_depths < 1 || c->num_depths > DAS_MAX_DEPTH) return DAS_ERR_SHAPE;
   if (c->num_layers < 1 || c->num_kv_heads < 1 || c->num_pages < 1) return DAS_ERR_SHAPE;
+  if (c->num_kv_heads > 65535) return DAS_ERR_SHAPE;
   if (c->num_k_planes < 1 || c->num_v_planes < 1) return DAS_ERR_SHAPE;
   if (c->head_dim != 64 && c->head_dim != 96 && c->head_dim != 128) return DAS_ERR_SHAPE;
   for (int r = 1; r <= c->num_depths; ++r) {
@@ -112,11 +113,24 @@ das_status make_plan(const das_cache *c, const das_batch *b, int hq, int w,
   if (plan->path == DAS_PATH_MFMA && pps > kMaxPagesPerSplit) pps = kMaxPagesPerSplit;
   plan->pages_per_split = pps;
   plan->nsplit = splits_of(maxp, pps);
-  // workgroups of one launch: (splits x KV heads x row tiles) per sequence
-  const long row_tiles = (plan->rows + 15) / 16;
-  const long wgs = static_cast<long>(b->batch) * c->num_kv_heads * plan->nsplit * row_tiles;
-  if (wgs > 0x7fffffffL || static_cast<long>(b->batch) * row_tiles > 65535)
-    return DAS_ERR_SHAPE;
+  // Every grid dimension of the launches stays within what HIP accepts:
+  // at most 2^32 - 1 work-items (workgroups x threads) per dimension.
+  const long long kMaxItems = 0xffffffffLL;
+  const long long units = static_cast<long long>(b->batch) * c->num_kv_heads;
+  if (plan->path == DAS_PATH_MFMA) {
+    const long long nq = mfma_tiles_per_wave(plan->rows), nw = mfma_waves(plan->rows);
+    const long long n_rt = (plan->rows + 16 * nq - 1) / (16 * nq);
+    const long long chunks = units * plan->nsplit * ((n_rt + nw - 1) / nw);
+    if (chunks * 64 * nw > kMaxItems) return DAS_ERR_SHAPE;
+  } else {
+    const long long n_rt = (plan->rows + valu_tile_rows(plan->rows) - 1) /
+                           valu_tile_rows(plan->rows);
+    // grid (splits, KV heads, sequences x row tiles) of 256-thread workgroups
+    if (static_cast<long long>(plan->nsplit) * 256 > kMaxItems ||
+        static_cast<long long>(b->batch) * n_rt > 65535)
+      return DAS_ERR_SHAPE;
+  }
+  if (units * 64 > kMaxItems) return DAS_ERR_SHAPE;  // the merge: (sequence, KV head) x 64
   const size_t per_split_rows =
       static_cast<size_t>(b->batch) * c->num_kv_heads * plan->nsplit * plan->rows;
   plan->nsplit_ml = (plan->nsplit + 3) & ~3;
@@ -259,12 +273,13 @@ das_status das_kv_append(const das_cache *cache, const das_batch *batch, const v
       !aligned(len_out, 4))
     return DAS_ERR_ALIGN;
   if (w_max < 1 || w_max > DAS_MAX_BLOCK) return DAS_ERR_SHAPE;
-  // (plane, layer, KV head) work units and the grid stay within int32
-  const long units = static_cast<long>(cache->num_k_planes > cache->num_v_planes
-                                           ? cache->num_k_planes
-                                           : cache->num_v_planes) *
-                     cache->num_layers * cache->num_kv_heads;
-  if (units > (1L << 28)) return DAS_ERR_SHAPE;
+  // The commit's grid: one wave per (plane, layer, KV head), four per
+  // 256-thread workgroup, keys and values in separate workgroups; at most
+  // 2^32 - 1 work-items along x.
+  const long long per_plane = static_cast<long long>(cache->num_layers) * cache->num_kv_heads;
+  const long long blocks = (cache->num_k_planes * per_plane + 3) / 4 +
+                           (cache->num_v_planes * per_plane + 3) / 4;
+  if (blocks * 256 > 0xffffffffLL) return DAS_ERR_SHAPE;
   if (len_out && static_cast<const void *>(len_out) ==
                      static_cast<const void *>(batch->prefix_len))
     return DAS_ERR_SHAPE;

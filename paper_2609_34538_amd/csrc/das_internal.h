@@ -49,6 +49,24 @@ struct AppendParams {
   int32_t batch, n_k_planes, n_v_planes, layers, hkv, num_pages, max_pages, w_max;
 };
 
+template <typename... KArgs>
+hipError_t launch_kernel_impl(void (*kernel)(KArgs...), dim3 grid, dim3 block, hipStream_t s,
+                              KArgs... args) {
+  void *argv[] = {static_cast<void *>(&args)...};
+  return hipLaunchKernel(reinterpret_cast<const void *>(kernel), grid, block, argv, 0, s);
+}
+
+// Enqueues kernel<<<grid, block, 0, s>>>(args...) and returns the status of
+// that launch alone: hipLaunchKernel reports it directly, so an error left
+// pending by the caller's earlier HIP work is neither taken for this launch's
+// nor cleared.
+template <typename... KArgs, typename... Args>
+hipError_t launch_kernel(void (*kernel)(KArgs...), dim3 grid, dim3 block, hipStream_t s,
+                         Args &&...args) {
+  static_assert(sizeof...(KArgs) == sizeof...(Args), "kernel argument count");
+  return launch_kernel_impl<KArgs...>(kernel, grid, block, s, static_cast<KArgs>(args)...);
+}
+
 // Launchers (return the hipError_t of the launch).
 hipError_t launch_attn_valu(const AttnParams &p, int dtype, int dh, hipStream_t s);
 hipError_t launch_attn_mfma(const AttnParams &p, int dh, hipStream_t s);
@@ -79,6 +97,14 @@ __host__ __device__ __forceinline__ int split_first_page(int s, int pps) {
 // at least 1 (the block's).
 __host__ __device__ __forceinline__ int splits_of(int npages, int pps) {
   return (npages + pps) / pps;
+}
+
+// Launch geometry of the matrix-core kernel for a block of `rows` query rows
+// (the launcher's template choice): 16-row tiles per wave and waves per
+// workgroup.
+__host__ __device__ constexpr int mfma_tiles_per_wave(int rows) { return rows <= 16 ? 1 : 2; }
+__host__ __device__ constexpr int mfma_waves(int rows) {
+  return rows <= 32 ? 1 : rows <= 64 ? 2 : 4;
 }
 
 // Query rows of one workgroup of the vector-ALU kernel: the smallest of 4, 8,

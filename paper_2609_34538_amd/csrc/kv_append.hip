@@ -203,8 +203,7 @@ hipError_t launch_typed(const AppendParams &p, hipStream_t s) {
   const int blocks = (p.n_k_planes * per_plane + kWaves - 1) / kWaves +
                      (p.n_v_planes * per_plane + kWaves - 1) / kWaves;
   dim3 grid(blocks, p.batch);
-  hipLaunchKernelGGL((kv_append_kernel<T, DH>), grid, dim3(64 * kWaves), 0, s, p);
-  return hipGetLastError();
+  return launch_kernel(kv_append_kernel<T, DH>, grid, dim3(64 * kWaves), s, p);
 }
 
 }  // namespace

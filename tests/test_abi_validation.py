@@ -210,8 +210,17 @@ def test_append_argument_checks():
     bad = make_cache()
     bad.head_dim = 100
     assert app(cc=bad) == SHAPE
+    # the commit's grid: 2 key planes + 1 value plane x L layers x 8 heads in
+    # workgroups of 4 waves = 6 L workgroups of 256 threads, at most 2^32 - 1
+    # work-items; at the limit validation passes (and the launch fails on a
+    # GPU-less host), one layer more is rejected
+    limit = (0xffffffff // 256) // 6
     big = make_cache()
-    big.num_layers = 1 << 26  # 2 key planes x 2^26 layers x 8 heads: past 2^28 work units
+    big.num_layers = limit
+    assert app(cc=big) == HIP
+    big.num_layers = limit + 1
+    assert app(cc=big) == SHAPE
+    big.num_layers = 1 << 26
     assert app(cc=big) == SHAPE
     nb = make_batch()
     nb.block_table = None
@@ -232,3 +241,25 @@ def test_greedy_accept_argument_checks():
     assert acc(m=FAKE + 1) == ALIGN
     assert acc(em=FAKE + 2) == ALIGN
     assert acc(err=FAKE + 3) == ALIGN
+
+
+def test_attention_grid_limits():
+    # matrix-core path, 8 query rows (one single-wave workgroup per chunk):
+    # 8 KV heads x nsplit chunks x 64 threads <= 2^32 - 1, nsplit = (maxp + 2) / 2
+    # at 2 pages per split
+    o = DasOptionsC()
+    o.path, o.pages_per_split = 2, 2
+    c = make_cache(hkv=8)
+    at = make_batch(B=1, maxp=2 * 8388607 - 2)
+    past = make_batch(B=1, maxp=2 * 8388608 - 2)
+    assert ws_bytes(c, at, hq=8, w=8, opts=o) > 0
+    assert ws_bytes(c, past, hq=8, w=8, opts=o) == 0
+    # vector-ALU path: the split count x 256 threads along x
+    o.path, o.pages_per_split = 1, 1
+    at = make_batch(B=1, maxp=(0xffffffff // 256) - 1)
+    past = make_batch(B=1, maxp=(0xffffffff // 256))
+    assert ws_bytes(c, at, hq=8, w=8, opts=o) > 0
+    assert ws_bytes(c, past, hq=8, w=8, opts=o) == 0
+    # KV heads: at most 65535
+    assert ws_bytes(make_cache(hkv=65535), make_batch(B=1, maxp=4), hq=65535, w=1) > 0
+    assert ws_bytes(make_cache(hkv=65536), make_batch(B=1, maxp=4), hq=65536, w=1) == 0
