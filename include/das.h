@@ -20,8 +20,10 @@
  * Conventions shared by every entry point
  * ---------------------------------------
  * - Ownership: every pointer is owned by the caller. The library allocates
- *   no device or host memory and frees nothing. Device pointers must stay
- *   valid until the enqueued work has completed on `stream`.
+ *   no device or host memory and frees nothing; its only device memory is
+ *   the fixed scratch array of das_attn_policy_noalloc (one per GPU, part of
+ *   the loaded code). Device pointers must stay valid until the enqueued
+ *   work has completed on `stream`.
  * - Asynchrony: calls only validate arguments and enqueue kernels on
  *   `stream`; they return before the GPU work runs. Device faults surface at
  *   the caller's next synchronisation of that stream.
@@ -37,8 +39,9 @@
  *   kernels OR bits into it (DAS_DEVERR_*) for out-of-range page ids,
  *   prefix lengths or commit counts, and skip the offending data instead of
  *   reading or writing out of bounds.
- * - Reentrancy: the library keeps no global state; calls from several host
- *   threads are safe. Concurrent calls that share a workspace or write the
+ * - Reentrancy: apart from the per-device scratch address of
+ *   das_attn_policy_noalloc (set once, under a lock) the library keeps no
+ *   global state; calls from several host threads are safe. Concurrent calls that share a workspace or write the
  *   same cache rows race on the device, as any two kernels writing the same
  *   memory would.
  * - Alignment: the kernels move K/V/Q/O rows with 16-byte accesses, so
@@ -230,6 +233,39 @@ das_status das_attn_policy(const das_cache *cache, const das_batch *batch,
                            void *out, float *lse,
                            void *workspace, size_t workspace_bytes,
                            const das_attn_options *opts, hipStream_t stream);
+
+/* Bytes of the library-owned scratch of das_attn_policy_noalloc (per GPU). */
+#define DAS_NOALLOC_SCRATCH_BYTES (64u << 20)
+
+/*
+ * das_attn_policy without a caller workspace, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation). The split partials go to a
+ * library-owned scratch array of DAS_NOALLOC_SCRATCH_BYTES bytes per GPU,
+ * placed when the library's code is loaded on that GPU and held until the
+ * process ends; this call allocates nothing. Results are those of
+ * das_attn_policy with the same arguments and `opts`, bit for bit.
+ *
+ * - The first call on a device (with that device current) looks up the
+ *   device address of that device's scratch copy; `stream` must belong to
+ *   the current device (DAS_ERR_UNSUPPORTED otherwise; NULL = the current
+ *   device's null stream).
+ * - DAS_ERR_WORKSPACE when the request's workspace
+ *   (das_attn_workspace_bytes_ex with the same arguments) exceeds
+ *   DAS_NOALLOC_SCRATCH_BYTES.
+ * - Every call on a GPU shares that GPU's scratch, and the scratch keeps
+ *   whatever the last call left there (nothing in it needs clearing: each
+ *   call writes every partial it reads). Calls that can overlap on one GPU
+ *   (on different streams, or from different threads without ordering)
+ *   race on it: serialise them on one stream, or use das_attn_policy with
+ *   separate workspaces.
+ */
+das_status das_attn_policy_noalloc(const das_cache *cache, const das_batch *batch,
+                                   int32_t layer, int32_t kappa, int32_t nu,
+                                   int32_t num_q_heads, int32_t block_len,
+                                   const void *q, const void *k_blk, const void *v_blk,
+                                   void *out, float *lse, const das_attn_options *opts,
+                                   hipStream_t stream);
 
 /*
  * Commit (Sec. 3.4; App. B.1): for each sequence b, write the full-depth K/V

@@ -24,6 +24,7 @@ LIB_PATH = os.environ.get("DAS_LIBRARY") or os.path.join(_HERE, "libdas.so")
 MAX_DEPTH = 64
 PAGE_TOKENS = 64
 MAX_BLOCK = 64
+NOALLOC_SCRATCH_BYTES = 64 << 20  # DAS_NOALLOC_SCRATCH_BYTES
 
 DAS_OK = 0
 STATUS_NAMES = {0: "DAS_OK", -1: "DAS_ERR_NULL", -2: "DAS_ERR_SHAPE", -3: "DAS_ERR_DEPTH",
@@ -34,7 +35,8 @@ PATHS = {"auto": 0, "valu": 1, "mfma": 2}
 DEVERR_PAGE, DEVERR_PREFIX, DEVERR_COMMIT, DEVERR_TESTED = 1, 2, 4, 8
 
 EXPORTED = ["das_attn_workspace_bytes", "das_attn_workspace_bytes_ex", "das_attn_draft_maturev",
-            "das_attn_verify", "das_attn_policy", "das_kv_append", "das_greedy_accept",
+            "das_attn_verify", "das_attn_policy", "das_attn_policy_noalloc", "das_kv_append",
+            "das_greedy_accept",
             "das_status_string", "das_version"]
 
 
@@ -80,6 +82,10 @@ def _load() -> ctypes.CDLL:
                                     c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
                                     c_size_t, po, c_void_p]
     lib.das_attn_policy.restype = c_int32
+    lib.das_attn_policy_noalloc.argtypes = [pc, pb, c_int32, c_int32, c_int32, c_int32,
+                                            c_int32, c_void_p, c_void_p, c_void_p, c_void_p,
+                                            c_void_p, po, c_void_p]
+    lib.das_attn_policy_noalloc.restype = c_int32
     lib.das_kv_append.argtypes = [pc, pb, c_void_p, c_void_p, c_int32, c_void_p, c_void_p,
                                   c_void_p]
     lib.das_kv_append.restype = c_int32
@@ -278,6 +284,28 @@ def attn_policy(cache: PagedCache, batch: Batch, layer: int, kappa: int, nu: int
                              workspace.numel(), ctypes.byref(o), _stream_handle(stream))
     if st != DAS_OK:
         raise DasError(st, "das_attn_policy")
+    return out
+
+
+def attn_policy_noalloc(cache: PagedCache, batch: Batch, layer: int, kappa: int, nu: int,
+                        q: torch.Tensor, k_blk: torch.Tensor, v_blk: torch.Tensor,
+                        out: torch.Tensor, lse: Optional[torch.Tensor] = None,
+                        path: str = "auto", pages_per_split: int = 0, stream=None) -> torch.Tensor:
+    """attn_policy without a workspace: the split partials go to the
+    library's fixed per-GPU scratch (das_attn_policy_noalloc). `out` must be
+    given, so the call allocates nothing."""
+    _check_block(cache, batch, q, k_blk, v_blk)
+    if out is None:
+        raise ValueError("out is required (the call allocates nothing)")
+    _check_outputs(cache, batch, q, out, lse)
+    o = _options(path, pages_per_split)
+    w, hq = q.shape[1], q.shape[2]
+    st = LIB.das_attn_policy_noalloc(ctypes.byref(cache.c), ctypes.byref(batch.c), layer, kappa,
+                                     nu, hq, w, q.data_ptr(), k_blk.data_ptr(), v_blk.data_ptr(),
+                                     out.data_ptr(), _ptr(lse), ctypes.byref(o),
+                                     _stream_handle(stream))
+    if st != DAS_OK:
+        raise DasError(st, "das_attn_policy_noalloc")
     return out
 
 

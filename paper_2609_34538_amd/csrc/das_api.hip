@@ -7,6 +7,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "das_internal.h"
 
 namespace das {
@@ -141,10 +143,12 @@ das_status make_plan(const das_cache *c, const das_batch *b, int hq, int w,
   return DAS_OK;
 }
 
-das_status attn_common(const das_cache *c, const das_batch *b, int layer, int kappa, int nu,
-                       int hq, int w, const void *q, const void *kb, const void *vb, void *out,
-                       float *lse, void *ws, size_t ws_bytes, const das_attn_options *o,
-                       hipStream_t stream) {
+// Validates an attention request and fills every launch parameter except the
+// workspace pointers. No HIP call.
+das_status prepare_attn(const das_cache *c, const das_batch *b, int layer, int kappa, int nu,
+                        int hq, int w, const void *q, const void *kb, const void *vb,
+                        void *out, float *lse, const das_attn_options *o, AttnParams *pp,
+                        Plan *plan) {
   das_status st = check_cache(c);
   if (st != DAS_OK) return st;
   st = check_batch(b);
@@ -158,16 +162,13 @@ das_status attn_common(const das_cache *c, const das_batch *b, int layer, int ka
   const int kplane = c->k_plane[kappa];
   const int vplane = c->v_plane[nu];
   if (kplane < 0 || vplane < 0) return DAS_ERR_DEPTH;
-  Plan plan;
-  st = make_plan(c, b, hq, w, o, &plan);
+  st = make_plan(c, b, hq, w, o, plan);
   if (st != DAS_OK) return st;
-  if (!ws || ws_bytes < plan.total) return DAS_ERR_WORKSPACE;
-  if (reinterpret_cast<uintptr_t>(ws) % kAlign != 0) return DAS_ERR_WORKSPACE;
 
   const int dh = c->head_dim;
   const size_t eb = static_cast<size_t>(elem_bytes(c->dtype));
   const size_t layer_elems = static_cast<size_t>(c->num_kv_heads) * c->num_pages * kPage * dh;
-  AttnParams p;
+  AttnParams &p = *pp;
   p.k_layer = static_cast<const char *>(c->k_pool) +
               (static_cast<size_t>(kplane) * c->num_layers + layer) * layer_elems * eb;
   p.v_layer = static_cast<const char *>(c->v_pool) +
@@ -180,33 +181,92 @@ das_status attn_common(const das_cache *c, const das_batch *b, int layer, int ka
   p.prefix_len = b->prefix_len;
   p.block_table = b->block_table;
   p.dev_error = b->dev_error;
-  char *wsb = static_cast<char *>(ws);
-  p.ws_o = reinterpret_cast<float *>(wsb);
-  p.ws_m = reinterpret_cast<float *>(wsb + plan.ws_o_bytes);
-  p.ws_l = reinterpret_cast<float *>(wsb + plan.ws_o_bytes + plan.ws_ml_bytes);
+  p.ws_o = p.ws_m = p.ws_l = nullptr;
   p.batch = b->batch;
   p.hq = hq;
   p.hkv = c->num_kv_heads;
   p.group = hq / c->num_kv_heads;
   p.w = w;
-  p.rows = plan.rows;
+  p.rows = plan->rows;
   p.num_pages = c->num_pages;
   p.max_pages = b->max_pages_per_seq;
-  p.pages_per_split = plan.pages_per_split;
-  p.nsplit = plan.nsplit;
-  p.nsplit_ml = plan.nsplit_ml;
+  p.pages_per_split = plan->pages_per_split;
+  p.nsplit = plan->nsplit;
+  p.nsplit_ml = plan->nsplit_ml;
   // log2(e) / sqrt(dh): logits are kept in base-2 units so exp2 can be used.
   const double log2e = 1.4426950408889634074;
   p.scale_log2 = static_cast<float>(log2e / __builtin_sqrt(static_cast<double>(dh)));
+  return DAS_OK;
+}
 
+// Enqueues a prepared request with its workspace (plan.total bytes at ws,
+// 256-byte aligned): the attention kernel, then the split merge when a
+// sequence can span several splits.
+das_status launch_attn(AttnParams p, const Plan &plan, int dtype, int dh, void *ws,
+                       hipStream_t stream) {
+  char *wsb = static_cast<char *>(ws);
+  p.ws_o = reinterpret_cast<float *>(wsb);
+  p.ws_m = reinterpret_cast<float *>(wsb + plan.ws_o_bytes);
+  p.ws_l = reinterpret_cast<float *>(wsb + plan.ws_o_bytes + plan.ws_ml_bytes);
   const bool mfma = plan.path == DAS_PATH_MFMA;
   const hipError_t e = mfma ? launch_attn_mfma(p, dh, stream)
-                            : launch_attn_valu(p, c->dtype, dh, stream);
+                            : launch_attn_valu(p, dtype, dh, stream);
   if (e != hipSuccess) return DAS_ERR_HIP;
   // one split per sequence: the attention kernel wrote every output itself
-  if (plan.nsplit > 1 && launch_attn_combine(p, c->dtype, dh, 1, stream) != hipSuccess)
+  if (plan.nsplit > 1 && launch_attn_combine(p, dtype, dh, 1, stream) != hipSuccess)
     return DAS_ERR_HIP;
   return DAS_OK;
+}
+
+das_status attn_common(const das_cache *c, const das_batch *b, int layer, int kappa, int nu,
+                       int hq, int w, const void *q, const void *kb, const void *vb, void *out,
+                       float *lse, void *ws, size_t ws_bytes, const das_attn_options *o,
+                       hipStream_t stream) {
+  AttnParams p;
+  Plan plan;
+  const das_status st = prepare_attn(c, b, layer, kappa, nu, hq, w, q, kb, vb, out, lse, o,
+                                     &p, &plan);
+  if (st != DAS_OK) return st;
+  if (!ws || ws_bytes < plan.total) return DAS_ERR_WORKSPACE;
+  if (reinterpret_cast<uintptr_t>(ws) % kAlign != 0) return DAS_ERR_WORKSPACE;
+  return launch_attn(p, plan, c->dtype, c->head_dim, ws, stream);
+}
+
+// ---------------------------------------------------------------------------
+// Library-owned scratch of the allocation-free attention entry point: one
+// copy per GPU, part of the code object (the loader places it when the
+// library's code is loaded on a device, and it lives until the process ends).
+// Host code never passes `scratch` itself to a kernel (in host code the name
+// stands for a host-side shadow, not a device address): the device address of
+// each GPU's copy is looked up once per device with hipGetSymbolAddress, with
+// that device current, and kept in scratch_ptr[].
+// ---------------------------------------------------------------------------
+constexpr int kMaxDevices = 64;
+__device__ __attribute__((aligned(256))) uint8_t scratch[DAS_NOALLOC_SCRATCH_BYTES];
+void *scratch_ptr[kMaxDevices];
+std::mutex scratch_mutex;
+
+// Device address of the current device's scratch copy, or nullptr.
+void *scratch_of_current_device(das_status *st) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) {
+    *st = DAS_ERR_HIP;
+    return nullptr;
+  }
+  if (dev >= kMaxDevices) {
+    *st = DAS_ERR_UNSUPPORTED;
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(scratch_mutex);
+  if (!scratch_ptr[dev]) {
+    void *ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) {
+      *st = DAS_ERR_HIP;
+      return nullptr;
+    }
+    scratch_ptr[dev] = ptr;
+  }
+  return scratch_ptr[dev];
 }
 
 }  // namespace
@@ -237,6 +297,29 @@ das_status das_attn_policy(const das_cache *cache, const das_batch *batch, int32
                            const das_attn_options *opts, hipStream_t stream) {
   return attn_common(cache, batch, layer, kappa, nu, num_q_heads, block_len, q, k_blk, v_blk,
                      out, lse, workspace, workspace_bytes, opts, stream);
+}
+
+das_status das_attn_policy_noalloc(const das_cache *cache, const das_batch *batch,
+                                   int32_t layer, int32_t kappa, int32_t nu,
+                                   int32_t num_q_heads, int32_t block_len, const void *q,
+                                   const void *k_blk, const void *v_blk, void *out, float *lse,
+                                   const das_attn_options *opts, hipStream_t stream) {
+  AttnParams p;
+  Plan plan;
+  das_status st = prepare_attn(cache, batch, layer, kappa, nu, num_q_heads, block_len, q,
+                               k_blk, v_blk, out, lse, opts, &p, &plan);
+  if (st != DAS_OK) return st;
+  if (plan.total > DAS_NOALLOC_SCRATCH_BYTES) return DAS_ERR_WORKSPACE;
+  // the stream must belong to the current device, whose scratch copy is used
+  if (stream) {
+    int cur = -1, sdev = -1;
+    if (hipGetDevice(&cur) != hipSuccess || hipStreamGetDevice(stream, &sdev) != hipSuccess)
+      return DAS_ERR_HIP;
+    if (sdev != cur) return DAS_ERR_UNSUPPORTED;
+  }
+  void *ws = scratch_of_current_device(&st);
+  if (!ws) return st;
+  return launch_attn(p, plan, cache->dtype, cache->head_dim, ws, stream);
 }
 
 das_status das_attn_draft_maturev(const das_cache *cache, const das_batch *batch,
