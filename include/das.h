@@ -148,11 +148,18 @@ typedef struct das_batch {
   uint32_t *dev_error;         /* optional device word (see DAS_DEVERR_*)     */
 } das_batch;
 
-/* Kernel family selection (measurement and tests). */
+/* Kernel family and schedule selection (measurement and tests). */
 typedef enum das_attn_path {
-  DAS_PATH_AUTO = 0,  /* library choice                                      */
-  DAS_PATH_VALU = 1,  /* vector-ALU kernel (the only path for fp32)          */
-  DAS_PATH_MFMA = 2   /* matrix-core kernel (bf16 only)                      */
+  DAS_PATH_AUTO = 0,     /* library choice                                   */
+  DAS_PATH_VALU = 1,     /* vector-ALU kernel (the only path for fp32)       */
+  DAS_PATH_MFMA = 2,     /* matrix-core kernel over prefix splits (bf16)     */
+  DAS_PATH_BALANCED = 3  /* matrix-core kernel, persistent balanced schedule:
+                            every resident wave streams an equal share of
+                            all sequences' tiles (bf16, 1..64 sequences,
+                            blocks of at most 32 query rows, i.e.
+                            w * Hq / Hkv <= 32, or 16 at head_dim 128;
+                            DAS_ERR_UNSUPPORTED otherwise). DAS_PATH_AUTO takes it for batches
+                            of 2..64 sequences when pages_per_split is 0. */
 } das_attn_path;
 
 typedef struct das_attn_options {
@@ -163,7 +170,7 @@ typedef struct das_attn_options {
                                clamped to the block table width + 1 (one
                                split then holds any sequence, and no merge
                                kernel runs), and to 64 on the matrix-core
-                               path                                          */
+                               path; not used by the balanced schedule      */
 } das_attn_options;
 
 /*

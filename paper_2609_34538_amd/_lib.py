@@ -31,7 +31,7 @@ STATUS_NAMES = {0: "DAS_OK", -1: "DAS_ERR_NULL", -2: "DAS_ERR_SHAPE", -3: "DAS_E
                 -4: "DAS_ERR_DTYPE", -5: "DAS_ERR_WORKSPACE", -6: "DAS_ERR_HIP",
                 -7: "DAS_ERR_UNSUPPORTED", -8: "DAS_ERR_ALIGN"}
 DTYPE_CODES = {torch.float32: 0, torch.bfloat16: 1}
-PATHS = {"auto": 0, "valu": 1, "mfma": 2}
+PATHS = {"auto": 0, "valu": 1, "mfma": 2, "balanced": 3}
 DEVERR_PAGE, DEVERR_PREFIX, DEVERR_COMMIT, DEVERR_TESTED = 1, 2, 4, 8
 
 EXPORTED = ["das_attn_workspace_bytes", "das_attn_workspace_bytes_ex", "das_attn_draft_maturev",

@@ -1,0 +1,531 @@
+// Balanced persistent matrix-core attention for batches of sequences with
+// different prefix lengths (Eq. (2)-(3) over a ragged batch).
+//
+// Work layout. A unit is one (sequence b, KV head) pair: its query block
+// (w * G <= 32 rows) against the sequence's prefix and the draft block. A
+// unit has 2 * ceil(S_b / 64) prefix tiles of 32 tokens (two per page) and
+// ceil(w / 32) block tiles, in that order. The units of all sequences, laid
+// end to end (sequence-major, then KV head), form one global sequence of T
+// tiles. Worker j of W (one single-wave workgroup per resident wave slot of
+// the chip) takes the tiles [T j / W, T (j + 1) / W): every worker streams
+// the same number of tiles (+-1), whatever the lengths, so the launch has no
+// tail of long chunks and no idle slots while short ones finish.
+//
+// A worker streams its tiles through a two-slot LDS ring (the direct-to-LDS
+// loads of the chunked kernel) without pausing at unit boundaries: while
+// tile k is computed, tile k + 1 is loaded into the other slot, and so are
+// the page id of tile k + 2 and, when tile k + 1 opens a new unit, that
+// unit's Q rows. One tile in flight per wave, all six waves of a compute
+// unit busy: on the batched workloads this measured faster than keeping two
+// tiles in flight (the chunked kernel's depth), 0.72-0.73 against 0.68-0.69
+// of 8 TB/s on the same box. At the end
+// of a unit (or of its range) the worker writes the unit's normalised output
+// when it processed the whole unit, otherwise an unnormalised piece
+// (m, l, O) that the merge kernel combines with the unit's other pieces.
+// Pieces are indexed unit + worker: along the tile sequence either the unit
+// or the worker (or both) advances, so the index is unique, and a unit's
+// pieces are consecutive.
+//
+// Both the attention kernel and the merge derive T, W and every unit's tile
+// range from the prefix lengths on the device (one length per lane, a wave
+// prefix sum), so the host needs no synchronisation. Batches of at most 64
+// sequences.
+
+#include "mfma_tile.h"
+
+namespace das {
+namespace {
+
+constexpr int kMinTilesPerWorker = 16;  // fewer tiles per worker: fewer workers
+
+__device__ __forceinline__ long long readlane64(long long x, int lane) {
+  const uint32_t lo = __builtin_amdgcn_readlane(static_cast<uint32_t>(x), lane);
+  const uint32_t hi = __builtin_amdgcn_readlane(static_cast<uint32_t>(x >> 32), lane);
+  return static_cast<long long>((static_cast<uint64_t>(hi) << 32) | lo);
+}
+
+// A wave-uniform pointer, held in scalar registers (the compiler cannot
+// always prove the uniformity of values carried across the loop, and a
+// buffer resource built from a vector register costs a waterfall loop).
+__device__ __forceinline__ const char *uniform_ptr(const char *ptr) {
+  const uint64_t v = reinterpret_cast<uint64_t>(ptr);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v));
+  const uint32_t hi = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(v >> 32));
+  return reinterpret_cast<const char *>((static_cast<uint64_t>(hi) << 32) | lo);
+}
+
+// Inclusive prefix sum over the wave's 64 lanes.
+__device__ __forceinline__ long long wave_incl_scan(long long x, int lane) {
+#pragma unroll
+  for (int d = 1; d < 64; d <<= 1) {
+    const long long y = __shfl_up(x, d, 64);
+    if (lane >= d) x += y;
+  }
+  return x;
+}
+
+// The tile numbering of one call, identical in the attention and the merge
+// kernels: lane b < B holds sequence b's clamped prefix length, its tiles
+// per unit and the inclusive prefix sum of the tiles of sequences 0..b.
+struct TileMap {
+  int s;            // lane b: prefix length S_b (clamped)
+  int tu;           // lane b: tiles per unit of sequence b
+  long long incl;   // lane b: tiles of the units of sequences 0..b
+  long long total;  // T
+  long long workers;  // W (wave-uniform)
+};
+
+__device__ __forceinline__ TileMap tile_map(const AttnParams &p, int lane, bool report) {
+  TileMap m;
+  const int s_raw = lane < p.batch ? p.prefix_len[lane] : 0;
+  bool bad;
+  m.s = clamp_prefix(s_raw, p.max_pages, &bad);
+  if (report && bad && lane < p.batch) report_error(p.dev_error, DAS_DEVERR_PREFIX);
+  m.tu = 2 * ((m.s + kPage - 1) / kPage) + ((p.w + 31) >> 5);
+  const long long own = lane < p.batch ? static_cast<long long>(m.tu) * p.hkv : 0;
+  m.incl = wave_incl_scan(own, lane);
+  m.total = readlane64(m.incl, 63);
+  long long w = m.total / kMinTilesPerWorker;
+  if (w < 1) w = 1;
+  m.workers = w < p.n_workers ? w : p.n_workers;
+  return m;
+}
+
+// The worker whose range holds global tile g: the largest j with
+// floor(T j / W) <= g.
+__device__ __forceinline__ long long worker_of(long long g, long long T, long long W) {
+  return ((g + 1) * W - 1) / T;
+}
+
+// Position of a worker in the tile sequence: unit (b, kvh), tile t of the
+// unit, and the unit's shape. Wave-uniform.
+struct Cursor {
+  int b, kvh, t;
+  int s, np, tu;  // prefix length, prefix pages, tiles of the unit
+};
+
+// The same cursor, pinned to scalar registers: values carried around the
+// tile loop are otherwise taken for divergent and kept (and branched on) in
+// vector registers.
+__device__ __forceinline__ Cursor uniform(const Cursor &x) {
+  Cursor y;
+  y.b = __builtin_amdgcn_readfirstlane(x.b);
+  y.kvh = __builtin_amdgcn_readfirstlane(x.kvh);
+  y.t = __builtin_amdgcn_readfirstlane(x.t);
+  y.s = __builtin_amdgcn_readfirstlane(x.s);
+  y.np = __builtin_amdgcn_readfirstlane(x.np);
+  y.tu = __builtin_amdgcn_readfirstlane(x.tu);
+  return y;
+}
+
+template <int DH, int NQ>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(2)))
+void attn_balanced_kernel(AttnParams p) {
+  using G = Geo<DH, NQ, 2>;
+  constexpr int KS = G::KS;
+  constexpr int DT = G::DT;
+  __shared__ __attribute__((aligned(16))) uint8_t ring[2 * G::SLOT];
+
+  const int lane = threadIdx.x;
+  const int ln = lane & 15;
+  const int lg = lane >> 4;
+  const int j = blockIdx.x;
+
+  const TileMap tm = tile_map(p, lane, j == 0);
+  if (j >= tm.workers) return;
+  const long long T = tm.total, W = tm.workers;
+  const long long g0 = T * j / W;
+  const long long n = T * (j + 1) / W - g0;  // >= 1: W <= max(1, T / 16)
+
+  // the unit holding g0: sequences ending at or before g0 come first
+  const uint64_t done = __builtin_amdgcn_ballot_w64(lane < p.batch && tm.incl <= g0);
+  Cursor c0;
+  c0.b = __builtin_amdgcn_readfirstlane(__builtin_popcountll(done));
+  c0.s = __builtin_amdgcn_readlane(tm.s, c0.b);
+  c0.np = (c0.s + kPage - 1) / kPage;
+  c0.tu = __builtin_amdgcn_readlane(tm.tu, c0.b);
+  {
+    const long long seq_start = readlane64(tm.incl, c0.b) -
+                                static_cast<long long>(c0.tu) * p.hkv;
+    const long long local = g0 - seq_start;
+    c0.kvh = static_cast<int>(local / c0.tu);
+    c0.t = static_cast<int>(local % c0.tu);
+  }
+  auto advance = [&](Cursor &x) {
+    if (++x.t < x.tu) return;
+    x.t = 0;
+    if (++x.kvh < p.hkv) return;
+    x.kvh = 0;
+    if (++x.b >= p.batch) return;  // past the last tile: never used
+    x.s = __builtin_amdgcn_readlane(tm.s, x.b);
+    x.np = (x.s + kPage - 1) / kPage;
+    x.tu = __builtin_amdgcn_readlane(tm.tu, x.b);
+  };
+
+  const char *kl = static_cast<const char *>(p.k_layer);
+  const char *vl = static_cast<const char *>(p.v_layer);
+  const size_t tok_bytes = static_cast<size_t>(p.hkv) * DH * 2;  // block row stride
+  // per-lane byte offsets of a fragment inside a page half (as in the
+  // chunked kernel): key token slot 8(n/4) + n%4, column 8g; value token
+  // group g, head dim n
+  const uint32_t lane_k = ((8 * (ln >> 2) + (ln & 3)) * DH + 8 * lg) * 2;
+  const uint32_t lane_v = (lg * DH + ln) * 16;
+
+  // page id of a prefix tile (0 for block tiles); read by every lane
+  auto load_pid = [&](const Cursor &x) -> int {
+    if (x.t >= 2 * x.np) return 0;
+    return p.block_table[static_cast<size_t>(x.b) * p.max_pages + (x.t >> 1)];
+  };
+  // Q fragments of a unit (B operand of S^T = K Q^T: lane holds dims
+  // 8g..8g+7 of row n); rows past the block's last are clamped and never
+  // written
+  auto load_q = [&](const Cursor &x, u32x4 (&qf)[NQ][KS]) {
+#pragma unroll
+    for (int qt = 0; qt < NQ; ++qt) {
+      const int row = min(qt * 16 + ln, p.rows - 1);
+      const int i = row / p.group, g = row % p.group;
+      const bf16_t *qrow = static_cast<const bf16_t *>(p.q) +
+                           ((static_cast<size_t>(x.b) * p.w + i) * p.hq + x.kvh * p.group + g) * DH;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+        qf[qt][ks] = *reinterpret_cast<const u32x4 *>(qrow + 32 * ks + 8 * lg);
+    }
+  };
+  // Sources of a tile: a prefix tile's 32-token key half and value half of
+  // its page; an out-of-range page id is reported and read as page 0 (the
+  // tile is then masked out).
+  auto tile_src = [&](const Cursor &x, int page, const char *&kbase, const char *&vbase,
+                      bool &ok) {
+    kbase = kl;
+    vbase = vl;
+    ok = true;
+    if (x.t >= 2 * x.np) return;
+    ok = page >= 0 && page < p.num_pages;
+    if (!ok) report_error(p.dev_error, DAS_DEVERR_PAGE);
+    const size_t off = (static_cast<size_t>(x.kvh) * p.num_pages + (ok ? page : 0)) *
+                       kPage * DH * 2;
+    const int u = x.t & 1;
+    kbase = kl + off + (32 * u) * DH * 2;
+    vbase = vl + off + 64 * DH * u;
+  };
+  // Loads of a tile into ring slot `si`, in three parts (key fragments of
+  // each S^T half, then the values) spread over the computation of the
+  // previous tile.
+  auto issue_part = [&](int si, const Cursor &x, int part, const char *kbase,
+                        const char *vbase) {
+    uint8_t *slot = ring + si * G::SLOT;
+    if (x.t < 2 * x.np) {
+      if (part < 2) {
+        const auto r = buffer_of(uniform_ptr(kbase), 64 * DH);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+          dma16(r, lane_k, (4 * part * DH + 32 * ks) * 2, slot + (part * KS + ks) * kFragBytes);
+      } else {
+        const auto r = buffer_of(uniform_ptr(vbase), 64 * DH);
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+          dma16(r, lane_v, 256 * dt, slot + (2 * KS + dt) * kFragBytes);
+      }
+    } else {
+      // draft block tile u: key fragments by token slot, value rows raw
+      const int u = x.t - 2 * x.np;
+      const size_t row0 = static_cast<size_t>(x.b) * p.w * p.hkv + x.kvh;
+      const char *kblk = static_cast<const char *>(p.kb) + row0 * DH * 2;
+      const char *vblk = static_cast<const char *>(p.vb) + row0 * DH * 2;
+      if (part < 2) {
+        const int tok = min(32 * u + 8 * (ln >> 2) + 4 * part + (ln & 3), p.w - 1);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+          dma16(kblk + tok * tok_bytes + (32 * ks + 8 * lg) * 2,
+                slot + (part * KS + ks) * kFragBytes);
+      } else {
+#pragma unroll
+        for (int f = 0; f < DT; ++f) {
+          const int o = f * kFragBytes + 16 * lane;  // byte in the [32][DH] half
+          const int tok = min(32 * u + o / (2 * DH), p.w - 1);
+          dma16(vblk + tok * tok_bytes + o % (2 * DH), slot + (2 * KS + f) * kFragBytes);
+        }
+      }
+    }
+  };
+
+  State<DH, NQ> st;
+  auto reset = [&]() {
+#pragma unroll
+    for (int qt = 0; qt < NQ; ++qt) {
+      st.m[qt] = kNegInf;
+      st.l[qt] = 0.f;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) st.o[qt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+  };
+  // End of a unit's stretch in this worker: the normalised output when the
+  // worker processed the whole unit, else a piece for the merge. Lane holds
+  // head dims 16dt + 4g .. +3 of row n of tile qt.
+  auto flush = [&](const Cursor &x, bool whole) {
+    const size_t piece = static_cast<size_t>(x.b) * p.hkv + x.kvh + j;
+#pragma unroll
+    for (int qt = 0; qt < NQ; ++qt) {
+      const int row = qt * 16 + ln;
+      if (row >= p.rows) continue;
+      if (whole) {
+        const float inv = 1.f / st.l[qt];
+        const int i = row / p.group, h = x.kvh * p.group + row % p.group;
+        bf16_t *orow = static_cast<bf16_t *>(p.out) +
+                       ((static_cast<size_t>(x.b) * p.w + i) * p.hq + h) * DH;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+          const f32x4 o = st.o[qt][dt];
+          u32x2 packed;
+          packed[0] = static_cast<uint32_t>(f32_to_bf16(o[0] * inv)) |
+                      (static_cast<uint32_t>(f32_to_bf16(o[1] * inv)) << 16);
+          packed[1] = static_cast<uint32_t>(f32_to_bf16(o[2] * inv)) |
+                      (static_cast<uint32_t>(f32_to_bf16(o[3] * inv)) << 16);
+          *reinterpret_cast<u32x2 *>(orow + 16 * dt + 4 * lg) = packed;
+        }
+        if (lg == 0 && p.lse)
+          p.lse[(static_cast<size_t>(x.b) * p.hq + h) * p.w + i] =
+              (st.m[qt] + log2f(st.l[qt])) * 0.69314718055994530942f;
+      } else {
+        float *orow = p.ws_o + (piece * p.rows + row) * DH;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+          *reinterpret_cast<f32x4 *>(orow + 16 * dt + 4 * lg) = st.o[qt][dt];
+        if (lg == 0) {
+          // -inf when no position was visible: weight 0 in the merge
+          p.ws_m[static_cast<size_t>(row) * p.piece_cap + piece] = st.m[qt];
+          p.ws_l[static_cast<size_t>(row) * p.piece_cap + piece] = st.l[qt];
+        }
+      }
+    }
+  };
+
+  // block position of each row (the causal cap on the block tiles)
+  int cap_blk[NQ];
+#pragma unroll
+  for (int qt = 0; qt < NQ; ++qt) cap_blk[qt] = (qt * 16 + ln) / p.group;
+
+  Cursor cc = c0;  // tile being computed
+  Cursor ci = c0;  // tile being issued
+  // A unit's Q rows are loaded while the tile before its first one is
+  // computed (into qn); with two row tiles per wave there is no room for the
+  // second set of registers, and they are loaded at the unit's first tile.
+  constexpr bool kPrefetchQ = NQ == 1;
+  u32x4 qf[NQ][KS], qn[kPrefetchQ ? NQ : 1][KS];
+  load_q(cc, qf);
+  const char *kbase, *vbase;
+  bool ok_cur, ok_next = true;
+  tile_src(ci, __builtin_amdgcn_readfirstlane(load_pid(ci)), kbase, vbase, ok_cur);
+  // the round trip (page id, Q) is complete before the first tile load, so
+  // the loop's waits count tile loads only
+  wait_vmcnt<0>();
+  for (int part = 0; part < 3; ++part) issue_part(0, ci, part, kbase, vbase);
+  advance(ci);
+  int pid_next = n > 1 ? load_pid(ci) : 0;  // page of tile 1
+  bool started_here = c0.t == 0;  // the worker holds its first unit's first tile
+  reset();
+
+  for (long long k = 0; k < n; ++k) {
+    wait_vmcnt<0>();  // tile k; the page id of tile k + 1; Q of tile k's unit
+    if (k > 0 && cc.t == 0) {
+      if constexpr (kPrefetchQ) {
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) qf[0][ks] = qn[0][ks];
+      } else {
+        load_q(cc, qf);
+      }
+    }
+    const uint8_t *slot = ring + (k & 1) * G::SLOT;
+    u32x4 kf[2][KS], vf[DT];
+#pragma unroll
+    for (int e = 0; e < 2; ++e)
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+        kf[e][ks] = *reinterpret_cast<const u32x4 *>(slot + (e * KS + ks) * kFragBytes + 16 * lane);
+    const bool prefix_tile = cc.t < 2 * cc.np;
+    int cap[NQ];
+    int limit;
+    bool full;
+    if (prefix_tile) {
+      limit = ok_cur ? min(32, cc.s - 32 * cc.t) : 0;
+      full = limit >= 32;
+#pragma unroll
+      for (int qt = 0; qt < NQ; ++qt) cap[qt] = 0x7fffffff;
+    } else {
+      const int u = cc.t - 2 * cc.np;
+      limit = p.w - 32 * u;
+      full = false;
+#pragma unroll
+      for (int qt = 0; qt < NQ; ++qt) cap[qt] = cap_blk[qt] - 32 * u;
+    }
+    // Every LDS read of the previous iteration (from the slot refilled
+    // below) and this tile's key fragments have completed.
+    __builtin_amdgcn_s_waitcnt(0xF | (0x3 << 14) | (0x7 << 4));  // lgkmcnt(0)
+    // The value fragments are read from LDS only before the P.V product, so
+    // they and the key fragments are never live together.
+    auto read_values = [&]() {
+      if (prefix_tile) {
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+          vf[dt] = *reinterpret_cast<const u32x4 *>(slot + (2 * KS + dt) * kFragBytes + 16 * lane);
+        if (!full) {
+          // invisible tokens enter P.V with probability 0; their values are
+          // zeroed so whatever the page holds there (NaN, Inf) adds nothing
+          const int nv = min(max(limit - 8 * lg, 0), 8);
+          u32x4 keep;
+#pragma unroll
+          for (int q4 = 0; q4 < 4; ++q4)
+            keep[q4] = (2 * q4 < nv ? 0xffffu : 0u) | (2 * q4 + 1 < nv ? 0xffff0000u : 0u);
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) vf[dt] &= keep;
+        }
+      } else {
+        // block values are token-major [32][DH] in the slot: gather V^T
+        const uint16_t *raw = reinterpret_cast<const uint16_t *>(slot + 2 * KS * kFragBytes);
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+          u16x8 v8;
+#pragma unroll
+          for (int jj = 0; jj < 8; ++jj) v8[jj] = raw[(8 * lg + jj) * DH + 16 * dt + ln];
+          vf[dt] = __builtin_bit_cast(u32x4, v8);
+        }
+      }
+    };
+
+    // tile k + 1 (= ci) goes to the other slot; its page id arrived with tile k
+    const bool refill = k + 1 < n;
+    if (refill) {
+      tile_src(ci, __builtin_amdgcn_readfirstlane(pid_next), kbase, vbase, ok_next);
+      if constexpr (kPrefetchQ)
+        if (ci.t == 0) load_q(ci, qn);  // tile k + 1 opens a unit
+    }
+    Cursor cn = ci;  // tile k + 2
+    advance(cn);
+    if (k + 2 < n) pid_next = load_pid(cn);
+    const int si = (k + 1) & 1;
+    compute_tile<DH, NQ>(st, kf, vf, qf, cap, limit, full, p.scale_log2, lg, [&](int part) {
+      if (refill) issue_part(si, ci, part, kbase, vbase);
+      if (part == 2) read_values();
+    });
+    const bool unit_end = cc.t == cc.tu - 1;
+    if (unit_end || k + 1 == n) {
+      flush(cc, started_here && unit_end);
+      started_here = true;  // every later unit starts inside this worker
+      reset();
+    }
+    cc = uniform(ci);
+    ci = uniform(cn);
+    ok_cur = ok_next;
+  }
+}
+
+// Merge of a unit's pieces (as the chunked kernel's merge, over the pieces
+// u + j of the workers j that share unit u). One single-wave workgroup per
+// (unit, 8 rows, 32 columns); units held by one worker exit at once.
+constexpr int kRowsPerBlock = 8;
+constexpr int kColsPerBlock = 32;
+constexpr int kEager = 8;
+
+template <typename T, int DH>
+__global__ __launch_bounds__(64) void attn_balanced_combine_kernel(AttnParams p) {
+  const int lane = threadIdx.x;
+  const TileMap tm = tile_map(p, lane, false);
+  const int unit = blockIdx.x;  // b * hkv + kvh
+  const int b = unit / p.hkv, kvh = unit % p.hkv;
+  const int tu = __builtin_amdgcn_readlane(tm.tu, b);
+  const long long s_u = readlane64(tm.incl, b) - static_cast<long long>(tu) * (p.hkv - kvh);
+  const long long jf = worker_of(s_u, tm.total, tm.workers);
+  const long long jl = worker_of(s_u + tu - 1, tm.total, tm.workers);
+  if (jf == jl) return;  // written by its worker
+  const int np = static_cast<int>(jl - jf + 1);
+
+  const int row = blockIdx.y * kRowsPerBlock + lane / 8;
+  const int c = blockIdx.z * kColsPerBlock + 4 * (lane % 8);
+  if (row >= p.rows || c >= DH) return;
+  const size_t piece0 = static_cast<size_t>(unit) + jf;
+  const float *mrow = p.ws_m + static_cast<size_t>(row) * p.piece_cap + piece0;
+  const float *lrow = p.ws_l + static_cast<size_t>(row) * p.piece_cap + piece0;
+  const float *orow = p.ws_o + (piece0 * p.rows + row) * DH + c;
+  const size_t ostride = static_cast<size_t>(p.rows) * DH;
+
+  float mv[kEager], lv[kEager];
+  float4 ov[kEager];
+#pragma unroll
+  for (int k = 0; k < kEager; ++k) {
+    const int kk = k < np ? k : 0;  // pieces past the count re-read the first
+    mv[k] = mrow[kk];
+    lv[k] = lrow[kk];
+    ov[k] = *reinterpret_cast<const float4 *>(orow + kk * ostride);
+  }
+  float mx = -__builtin_huge_valf();
+#pragma unroll
+  for (int k = 0; k < kEager; ++k) mx = k < np ? fmaxf(mx, mv[k]) : mx;
+  float den = 0.f, n0 = 0.f, n1 = 0.f, n2 = 0.f, n3 = 0.f;
+#pragma unroll
+  for (int k = 0; k < kEager; ++k) {
+    if (k < np) {
+      const float sc = exp2f(mv[k] - mx);
+      den += sc * lv[k];
+      n0 += sc * ov[k].x;
+      n1 += sc * ov[k].y;
+      n2 += sc * ov[k].z;
+      n3 += sc * ov[k].w;
+    }
+  }
+  for (int k = kEager; k < np; ++k) {
+    const float m = mrow[k], l = lrow[k];
+    const float4 o = *reinterpret_cast<const float4 *>(orow + k * ostride);
+    const float nm = fmaxf(mx, m);
+    const float a = exp2f(mx - nm), sc = exp2f(m - nm);
+    den = den * a + sc * l;
+    n0 = n0 * a + sc * o.x;
+    n1 = n1 * a + sc * o.y;
+    n2 = n2 * a + sc * o.z;
+    n3 = n3 * a + sc * o.w;
+    mx = nm;
+  }
+  const int i = row / p.group, h = kvh * p.group + row % p.group;
+  T *out = static_cast<T *>(p.out) + ((static_cast<size_t>(b) * p.w + i) * p.hq + h) * DH + c;
+  const float inv = 1.f / den;
+  out[0] = from_f32<T>(n0 * inv);
+  out[1] = from_f32<T>(n1 * inv);
+  out[2] = from_f32<T>(n2 * inv);
+  out[3] = from_f32<T>(n3 * inv);
+  if (p.lse && c == 0)
+    p.lse[(static_cast<size_t>(b) * p.hq + h) * p.w + i] =
+        (mx + log2f(den)) * 0.69314718055994530942f;
+}
+
+// Blocks of up to 16 query rows: one row tile per wave; 17..32 rows: two
+// (head dims 64 and 96 only: at 128 the second tile does not fit in the
+// wave's registers, and such requests keep the split grid).
+template <int DH>
+hipError_t launch_dh(const AttnParams &p, hipStream_t s) {
+  const dim3 grid(static_cast<unsigned>(p.n_workers));
+  static_assert(balanced_max_rows(DH) == (DH == 128 ? 16 : 32), "launch shapes");
+  if (p.rows <= 16) return launch_kernel(attn_balanced_kernel<DH, 1>, grid, dim3(64), s, p);
+  if constexpr (DH == 128) return hipErrorInvalidValue;
+  else return launch_kernel(attn_balanced_kernel<DH, 2>, grid, dim3(64), s, p);
+}
+
+template <int DH>
+hipError_t launch_combine_dh(const AttnParams &p, hipStream_t s) {
+  const dim3 grid(p.batch * p.hkv, (p.rows + kRowsPerBlock - 1) / kRowsPerBlock,
+                  (DH + kColsPerBlock - 1) / kColsPerBlock);
+  return launch_kernel(attn_balanced_combine_kernel<bf16_t, DH>, grid, dim3(64), s, p);
+}
+
+}  // namespace
+
+hipError_t launch_attn_balanced(const AttnParams &p, int dh, hipStream_t s) {
+  hipError_t e;
+  if (dh == 64) e = launch_dh<64>(p, s);
+  else if (dh == 96) e = launch_dh<96>(p, s);
+  else e = launch_dh<128>(p, s);
+  if (e != hipSuccess) return e;
+  if (dh == 64) return launch_combine_dh<64>(p, s);
+  if (dh == 96) return launch_combine_dh<96>(p, s);
+  return launch_combine_dh<128>(p, s);
+}
+
+}  // namespace das

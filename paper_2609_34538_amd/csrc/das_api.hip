@@ -52,11 +52,18 @@ das_status check_batch(const das_batch *b) {
   return DAS_OK;
 }
 
-// Which kernel family runs a request.
-int choose_path(const das_cache *c, const das_attn_options *o) {
+// Which kernel family (and schedule) runs a request. The balanced schedule
+// serves ragged batches: every resident wave streams an equal share of all
+// tiles, so unequal prefix lengths leave no idle slots; a single sequence
+// has nothing to balance and keeps the split grid (one fewer dependent
+// memory round trip before its first tile).
+int choose_path(const das_cache *c, const das_batch *b, int rows, const das_attn_options *o) {
   const int want = o ? o->path : DAS_PATH_AUTO;
   if (c->dtype == DAS_F32) return DAS_PATH_VALU;
-  if (want == DAS_PATH_VALU || want == DAS_PATH_MFMA) return want;
+  if (want != DAS_PATH_AUTO) return want;
+  if (b->batch >= 2 && b->batch <= kBalancedMaxBatch && rows <= balanced_max_rows(c->head_dim) &&
+      !(o && o->pages_per_split != 0))
+    return DAS_PATH_BALANCED;
   return DAS_PATH_MFMA;
 }
 
@@ -66,6 +73,8 @@ struct Plan {
   int pages_per_split;
   int nsplit;
   int nsplit_ml;        // nsplit rounded up to a multiple of 4
+  int n_workers;        // balanced schedule: workers launched
+  int piece_cap;        // balanced schedule: pieces the workspace holds
   size_t ws_o_bytes, ws_ml_bytes, total;
 };
 
@@ -84,11 +93,33 @@ das_status make_plan(const das_cache *c, const das_batch *b, int hq, int w,
   const int group = hq / c->num_kv_heads;
   if (group > 8) return DAS_ERR_UNSUPPORTED;
   if (w < 1 || w > DAS_MAX_BLOCK) return DAS_ERR_SHAPE;
-  if (o && (o->pages_per_split < 0 || o->path < DAS_PATH_AUTO || o->path > DAS_PATH_MFMA))
+  if (o && (o->pages_per_split < 0 || o->path < DAS_PATH_AUTO || o->path > DAS_PATH_BALANCED))
     return DAS_ERR_SHAPE;
-  if (o && o->path == DAS_PATH_MFMA && c->dtype != DAS_BF16) return DAS_ERR_UNSUPPORTED;
-  plan->path = choose_path(c, o);
+  if (o && (o->path == DAS_PATH_MFMA || o->path == DAS_PATH_BALANCED) && c->dtype != DAS_BF16)
+    return DAS_ERR_UNSUPPORTED;
   plan->rows = w * group;
+  plan->path = choose_path(c, b, plan->rows, o);
+  if (plan->path == DAS_PATH_BALANCED) {
+    if (b->batch > kBalancedMaxBatch || plan->rows > balanced_max_rows(c->head_dim))
+      return DAS_ERR_UNSUPPORTED;
+    // workers: one per resident single-wave workgroup of the chip; pieces:
+    // at most units + workers - 1 (index unit + worker)
+    plan->n_workers = kNumCUs * balanced_workers_per_cu(c->head_dim);
+    plan->piece_cap = b->batch * c->num_kv_heads + plan->n_workers;
+    plan->pages_per_split = 0;
+    plan->nsplit = 0;
+    plan->nsplit_ml = 0;
+    const size_t pieces = static_cast<size_t>(plan->piece_cap);
+    plan->ws_o_bytes = align_up(pieces * plan->rows * c->head_dim * sizeof(float));
+    plan->ws_ml_bytes = align_up(pieces * plan->rows * sizeof(float));
+    plan->total = plan->ws_o_bytes + 2 * plan->ws_ml_bytes;
+    // merge grid: (sequence, KV head) x 64 threads along x
+    if (static_cast<long long>(b->batch) * c->num_kv_heads * 64 > 0xffffffffLL)
+      return DAS_ERR_SHAPE;
+    return DAS_OK;
+  }
+  plan->n_workers = 0;
+  plan->piece_cap = 0;
   const int maxp = b->max_pages_per_seq;
   int pps = o ? o->pages_per_split : 0;
   if (pps == 0) {
@@ -193,6 +224,8 @@ das_status prepare_attn(const das_cache *c, const das_batch *b, int layer, int k
   p.pages_per_split = plan->pages_per_split;
   p.nsplit = plan->nsplit;
   p.nsplit_ml = plan->nsplit_ml;
+  p.n_workers = plan->n_workers;
+  p.piece_cap = plan->piece_cap;
   // log2(e) / sqrt(dh): logits are kept in base-2 units so exp2 can be used.
   const double log2e = 1.4426950408889634074;
   p.scale_log2 = static_cast<float>(log2e / __builtin_sqrt(static_cast<double>(dh)));
@@ -208,6 +241,8 @@ das_status launch_attn(AttnParams p, const Plan &plan, int dtype, int dh, void *
   p.ws_o = reinterpret_cast<float *>(wsb);
   p.ws_m = reinterpret_cast<float *>(wsb + plan.ws_o_bytes);
   p.ws_l = reinterpret_cast<float *>(wsb + plan.ws_o_bytes + plan.ws_ml_bytes);
+  if (plan.path == DAS_PATH_BALANCED)
+    return launch_attn_balanced(p, dh, stream) == hipSuccess ? DAS_OK : DAS_ERR_HIP;
   const bool mfma = plan.path == DAS_PATH_MFMA;
   const hipError_t e = mfma ? launch_attn_mfma(p, dh, stream)
                             : launch_attn_valu(p, dtype, dh, stream);

@@ -34,6 +34,10 @@ struct AttnParams {
   int32_t pages_per_split, nsplit;
   int32_t nsplit_ml;     // nsplit rounded up to a multiple of 4 (16-byte rows of m, l)
   float scale_log2;      // log2(e) / sqrt(dh): logits in base-2 units
+  // balanced schedule only: workers launched (one single-wave workgroup
+  // each) and the piece capacity of the workspace (ws_o [piece_cap][rows][dh],
+  // ws_m / ws_l [rows][piece_cap])
+  int32_t n_workers, piece_cap;
 };
 
 struct AppendParams {
@@ -75,6 +79,20 @@ hipError_t launch_attn_mfma(const AttnParams &p, int dh, hipStream_t s);
 hipError_t launch_attn_combine(const AttnParams &p, int dtype, int dh, int skip_single,
                                hipStream_t s);
 hipError_t launch_kv_append(const AppendParams &p, int dtype, int dh, hipStream_t s);
+// Balanced persistent schedule for batches of up to 64 sequences with blocks
+// of at most balanced_max_rows(dh) query rows (bf16): the attention kernel
+// and its piece merge.
+hipError_t launch_attn_balanced(const AttnParams &p, int dh, hipStream_t s);
+constexpr int kBalancedMaxBatch = 64;
+// query rows per (sequence, KV head) the balanced kernel takes
+__host__ __device__ constexpr int balanced_max_rows(int dh) { return dh == 128 ? 16 : 32; }
+constexpr int kNumCUs = 256;  // compute units of an MI355X (gfx950)
+// Workers of the balanced schedule per compute unit: as many of its
+// single-wave workgroups as the 160 KB of LDS hold (two ring slots of
+// 2 * dh / 32 + dh / 16 one-KB fragments each).
+__host__ __device__ constexpr int balanced_workers_per_cu(int dh) {
+  return (160 * 1024) / (2 * (2 * (dh / 32) + dh / 16) * 1024);
+}
 
 struct AcceptParams {
   const int32_t *proposals;    // [B][w]

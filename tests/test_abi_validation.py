@@ -263,3 +263,39 @@ def test_attention_grid_limits():
     # KV heads: at most 65535
     assert ws_bytes(make_cache(hkv=65535), make_batch(B=1, maxp=4), hq=65535, w=1) > 0
     assert ws_bytes(make_cache(hkv=65536), make_batch(B=1, maxp=4), hq=65536, w=1) == 0
+
+
+def test_balanced_schedule_workspace_and_limits():
+    # pieces = sequences x KV heads + workers (256 CUs x the single-wave
+    # workgroups whose two ring slots fit in 160 KB: 6 at head dim 96, 5 at 128)
+    o = DasOptionsC()
+    o.path, o.pages_per_split = 3, 0
+    al = lambda x: (x + 255) // 256 * 256
+    c, b = make_cache(hkv=8, dh=96), make_batch(B=4, maxp=10)
+    rows = 16 * 2  # w 16, G 2
+    pieces = 4 * 8 + 256 * 6
+    assert ws_bytes(c, b, hq=16, w=16, opts=o) == al(pieces * rows * 96 * 4) + 2 * al(pieces * rows * 4)
+    c128 = make_cache(hkv=8, dh=128)
+    pieces = 4 * 8 + 256 * 5
+    assert ws_bytes(c128, b, hq=8, w=16, opts=o) == al(pieces * 16 * 128 * 4) + 2 * al(pieces * 16 * 4)
+    # limits: 64 sequences, 32 query rows (16 at head dim 128)
+    assert ws_bytes(c, make_batch(B=64, maxp=10), hq=8, w=32, opts=o) > 0
+    assert ws_bytes(c, make_batch(B=65, maxp=10), hq=8, w=32, opts=o) == 0
+    assert ws_bytes(c, b, hq=8, w=33, opts=o) == 0
+    assert ws_bytes(c128, b, hq=8, w=17, opts=o) == 0
+    # library choice: the balanced schedule for 2..64 sequences, the split
+    # grid otherwise (its workspace is sized per split)
+    o.path = 0
+    assert ws_bytes(c, b, hq=16, w=16, opts=o) == ws_bytes(c, b, hq=16, w=16, opts=_opts(3))
+    assert ws_bytes(c, make_batch(B=1), hq=16, w=16, opts=o) == \
+        ws_bytes(c, make_batch(B=1), hq=16, w=16, opts=_opts(2))
+    o.pages_per_split = 4
+    assert ws_bytes(c, b, hq=16, w=16, opts=o) == ws_bytes(c, b, hq=16, w=16, opts=_opts(2, 4))
+    # fp32 caches have no balanced schedule
+    assert ws_bytes(make_cache(dtype=0), b, opts=_opts(3)) == 0
+
+
+def _opts(path, pps=0):
+    o = DasOptionsC()
+    o.path, o.pages_per_split = path, pps
+    return o

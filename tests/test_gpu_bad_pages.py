@@ -53,7 +53,8 @@ def _expected(cd, wl, layer, kappa, nu, q, kb, vb, bad):
     return np.stack(outs)
 
 
-@pytest.mark.parametrize("path,pps", [("valu", 1), ("valu", 2), ("mfma", 2), ("mfma", 3)])
+@pytest.mark.parametrize("path,pps", [("valu", 1), ("valu", 2), ("mfma", 2), ("mfma", 3),
+                                      ("balanced", 0)])
 @pytest.mark.parametrize("low", [False, True], ids=["random", "low-logits"])
 def test_bad_page_ids_are_skipped_and_reported(path, pps, low):
     wl, cd, table, bad = _case(low)

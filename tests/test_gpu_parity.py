@@ -37,12 +37,24 @@ def small_workloads():
 EDGE_LENS = {"c3s": [0, 1, 63, 64, 65, 300]}
 
 
-# kernel family of a parametrised case
-KERNELS = {"valu": dict(path="valu"), "mfma": dict(path="mfma")}
+# kernel family (and schedule) of a parametrised case
+KERNELS = {"valu": dict(path="valu"), "mfma": dict(path="mfma"),
+           "balanced": dict(path="balanced")}
+
+
+def balanced_ok(wl, widths=None, batch=None):
+    """The balanced schedule takes up to 64 sequences and blocks of at most
+    32 query rows (16 at head dim 128)."""
+    widths = widths if widths is not None else list(wl.draft_widths) + [wl.verify_width]
+    limit = 16 if wl.dh == 128 else 32
+    return ((batch or wl.batch) <= 64 and max(widths) * wl.group <= limit
+            and wl.dtype == torch.bfloat16)
 
 
 def _paths(wl):
-    return ["valu"] if wl.dtype == torch.float32 else list(KERNELS)
+    if wl.dtype == torch.float32:
+        return ["valu"]
+    return ["valu", "mfma"] + (["balanced"] if balanced_ok(wl) else [])
 
 
 def _cases():
@@ -104,10 +116,12 @@ def test_split_sizes_agree_with_oracle(small_data, path, pps):
 
 
 @pytest.mark.parametrize("path", list(KERNELS))
-@pytest.mark.parametrize("w", [1, 2, 3, 7, 17, 33, 64])
+@pytest.mark.parametrize("w", [1, 2, 3, 7, 17, 32, 33, 64])
 def test_block_widths(small_data, w, path):
     cd = small_data["c5s"]
     wl = cd.wl
+    if path == "balanced" and not balanced_ok(wl, [w]):
+        pytest.skip("blocks of more than 32 query rows take the split grid")
     cache, batch = wrap(cd)
     q, kb, vb = dg.block_inputs(cd, w, 3, DEV)
     out = das.attn_policy(cache, batch, 0, 3, wl.depth_R, q, kb, vb, **KERNELS[path])
@@ -138,7 +152,7 @@ def test_entry_points_are_policy_corners(small_data):
 
 @pytest.mark.parametrize("path", list(KERNELS))
 def test_deterministic(small_data, path):
-    cd = small_data["c4s"]
+    cd = small_data["c4s" if path != "balanced" else "c5s"]
     wl = cd.wl
     cache, batch = wrap(cd)
     q, kb, vb = dg.block_inputs(cd, 32, 3, DEV)
@@ -193,7 +207,8 @@ def _poison_past_prefix(cd: dg.CacheData):
 
 
 @pytest.mark.parametrize("name,path", [("c3s", "valu"), ("c3s", "mfma"), ("c1", "valu"),
-                                       ("gqa8_w32", "mfma"), ("c5s", "mfma")])
+                                       ("gqa8_w32", "mfma"), ("c5s", "mfma"),
+                                       ("c3s", "balanced"), ("c5s", "balanced")])
 def test_non_finite_cache_past_the_prefix_is_ignored(name, path):
     """Positions past a sequence's prefix enter the softmax with probability
     0; whatever the cache holds there (here NaN and Inf) must contribute

@@ -1,4 +1,4 @@
-"""Seeded random shapes through both kernel families against the fp64
+"""Seeded random shapes through every kernel family and schedule against the fp64
 oracle: batch, GQA group, head dim, block width, read depths, ragged prefix
 lengths (empty, page boundaries, ragged tails) and explicit split sizes."""
 
@@ -44,7 +44,10 @@ def test_random_shapes(seed):
     w = wl.draft_widths[0]
     q, kb, vb = dg.block_inputs(cd, w, kappa, DEV)
     ref, ref_lse = oracle_call(cd, 1, kappa, nu, q, kb, vb, range(wl.batch))
-    for path in ("valu", "mfma"):
+    paths = ["valu", "mfma"]
+    if wl.batch <= 64 and w * wl.group <= (16 if wl.dh == 128 else 32):
+        paths.append("balanced")
+    for path in paths:
         lse = torch.empty((wl.batch, wl.hq, w), dtype=torch.float32, device=DEV)
         out = das.attn_policy(cache, batch, 1, kappa, nu, q, kb, vb, lse=lse, path=path,
                               pages_per_split=pps)

@@ -25,7 +25,7 @@ def _inputs(wl, lens, w, d):
 
 
 @pytest.mark.parametrize("dtype,path", [(torch.bfloat16, "mfma"), (torch.bfloat16, "valu"),
-                                        (torch.float32, "valu")])
+                                        (torch.bfloat16, "balanced"), (torch.float32, "valu")])
 def test_noalloc_matches_policy_on_two_calls(dtype, path):
     big = dg.scaled(dg.WORKLOADS[5], dtype=dtype, batch=5, hq=8, hkv=4, layers=2,
                     prefix=(0, 0), draft_widths=(16,), verify_width=16)
@@ -60,10 +60,12 @@ def test_noalloc_rejects_requests_beyond_the_scratch():
     cache = das.PagedCache(k_pool, v_pool, 32, {32: 0}, {32: 0})
     batch = das.Batch(torch.zeros(32, dtype=torch.int32, device=DEV),
                       torch.zeros((32, 129), dtype=torch.int32, device=DEV))
-    assert das.workspace_bytes(cache, batch, hkv, w) > das.NOALLOC_SCRATCH_BYTES
+    # on the split grid (the balanced schedule's pieces fit)
+    assert das.workspace_bytes(cache, batch, hkv, w, path="mfma") > das.NOALLOC_SCRATCH_BYTES
+    assert das.workspace_bytes(cache, batch, hkv, w) <= das.NOALLOC_SCRATCH_BYTES
     q = torch.zeros((32, w, hkv, dh), dtype=torch.bfloat16, device=DEV)
     kb = torch.zeros((32, w, hkv, dh), dtype=torch.bfloat16, device=DEV)
     out = torch.empty_like(q)
     with pytest.raises(das.DasError) as e:
-        das.attn_policy_noalloc(cache, batch, 0, 32, 32, q, kb, kb, out)
+        das.attn_policy_noalloc(cache, batch, 0, 32, 32, q, kb, kb, out, path="mfma")
     assert e.value.status == -5  # DAS_ERR_WORKSPACE
