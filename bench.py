@@ -43,15 +43,21 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0
 
-# HBM bytes per attention launch (kernel + split merge) from rocprofv3
-# FETCH_SIZE / WRITE_SIZE passes over this benchmark's default command, each
-# scaled by what the counter reads for a plain 1 GiB copy; valid only for the
-# kernel sources with this digest, the default workload and library plan.
-MEASURED_TRAFFIC = {("single-seq-looped-bf16", "eee63ebbb572754b"): 47_900_635}
+# HBM bytes per attention launch (attention kernel + split merge, averaged
+# over a step's launches) from rocprofv3 FETCH_SIZE / WRITE_SIZE passes over
+# this benchmark's command for each workload, each counter scaled by what it
+# reads for a plain 1 GiB device copy; valid only for the kernel sources with
+# this digest and the library's default plan.
 TRAFFIC_SOURCES = ["paper_2609_34538_amd/csrc/attn_mfma.hip",
+                   "paper_2609_34538_amd/csrc/attn_balanced.hip",
                    "paper_2609_34538_amd/csrc/attn_combine.hip",
+                   "paper_2609_34538_amd/csrc/mfma_tile.h",
                    "paper_2609_34538_amd/csrc/das_api.hip",
                    "paper_2609_34538_amd/csrc/das_internal.h"]
+MEASURED_TRAFFIC = {("das-wave-step-bf16", "93951a37267e7167"): 4_512_325_279,
+                    ("long-prefix-gqa-bf16", "93951a37267e7167"): 344_385_565,
+                    ("ragged-paged-bf16", "93951a37267e7167"): 859_773_684,
+                    ("single-seq-looped-bf16", "93951a37267e7167"): 47_885_685}
 
 
 def kernel_digest():
