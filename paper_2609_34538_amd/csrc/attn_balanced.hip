@@ -179,6 +179,12 @@ void attn_balanced_kernel(AttnParams p) {
   // Q fragments of a unit (B operand of S^T = K Q^T: lane holds dims
   // 8g..8g+7 of row n); rows past the block's last are clamped and never
   // written
+  auto q_row = [&](const Cursor &x, int qt) {
+    const int row = min(qt * 16 + ln, p.rows - 1);
+    const int i = row / p.group, g = row % p.group;
+    return static_cast<const bf16_t *>(p.q) +
+           ((static_cast<size_t>(x.b) * p.w + i) * p.hq + x.kvh * p.group + g) * DH;
+  };
   auto load_q = [&](const Cursor &x, u32x4 (&qf)[NQ][KS]) {
 #pragma unroll
     for (int qt = 0; qt < NQ; ++qt) {
@@ -305,69 +311,92 @@ void attn_balanced_kernel(AttnParams p) {
 #pragma unroll
   for (int qt = 0; qt < NQ; ++qt) cap_blk[qt] = (qt * 16 + ln) / p.group;
 
-  Cursor cc = c0;  // tile being computed
-  Cursor ci = c0;  // tile being issued
-  // A unit's Q rows are loaded while the tile before its first one is
-  // computed (into qn); with two row tiles per wave there is no room for the
-  // second set of registers, and they are loaded at the unit's first tile.
+  // Page ids of the sequence of the current unit, 64 at a time: lane i holds
+  // the id of page pw0 + i (0 past the table's width).
+  auto load_window = [&](int b, int pw0) -> int {
+    const int pg = pw0 + lane;
+    return pg < p.max_pages ? p.block_table[static_cast<size_t>(b) * p.max_pages + pg] : 0;
+  };
+  auto next_unit = [&](const Cursor &x) {
+    Cursor y = x;
+    y.t = 0;
+    if (++y.kvh == p.hkv) {
+      y.kvh = 0;
+      ++y.b;
+      y.s = __builtin_amdgcn_readlane(tm.s, y.b);
+      y.np = (y.s + kPage - 1) / kPage;
+      y.tu = __builtin_amdgcn_readlane(tm.tu, y.b);
+    }
+    return uniform(y);
+  };
+
+  // Outer loop: the units of this worker's range; inner loop: the unit's
+  // tiles in the range, tile t computed while tile t + 1 (or the next unit's
+  // first tile) is loaded into the other ring slot. The next unit's Q rows
+  // and first page window, and the current unit's next page window, are
+  // loaded one window or one unit ahead; the wait at the top of every tile
+  // completes them with the tile.
+  Cursor cu = c0;
+  int pw0 = (c0.t >> 1) & ~63;
+  int pwin = load_window(cu.b, pw0);
+  int x_pw0 = -1;  // first page of the prefetched next window (-1: none)
+  int pwin_x = 0;
+  if (pw0 + 64 < cu.np) {
+    x_pw0 = pw0 + 64;
+    pwin_x = load_window(cu.b, x_pw0);
+  }
+  // With one row tile per wave the next unit's Q rows are loaded at the
+  // start of the current unit (qn); with two there is no room for a second
+  // set, and they are loaded when the unit starts (one round trip per unit).
   constexpr bool kPrefetchQ = NQ == 1;
   u32x4 qf[NQ][KS], qn[kPrefetchQ ? NQ : 1][KS];
-  load_q(cc, qf);
-  const char *kbase, *vbase;
-  bool ok_cur, ok_next = true;
-  tile_src(ci, __builtin_amdgcn_readfirstlane(load_pid(ci)), kbase, vbase, ok_cur);
-  // the round trip (page id, Q) is complete before the first tile load, so
-  // the loop's waits count tile loads only
+  load_q(cu, qf);
   wait_vmcnt<0>();
-  for (int part = 0; part < 3; ++part) issue_part(0, ci, part, kbase, vbase);
-  advance(ci);
-  int pid_next = n > 1 ? load_pid(ci) : 0;  // page of tile 1
-  bool started_here = c0.t == 0;  // the worker holds its first unit's first tile
-  reset();
-
-  for (long long k = 0; k < n; ++k) {
-    wait_vmcnt<0>();  // tile k; the page id of tile k + 1; Q of tile k's unit
-    if (k > 0 && cc.t == 0) {
+  const char *kbase, *vbase;
+  bool ok_cur;
+  {
+    const int pg = cu.t >> 1;
+    tile_src(cu, __builtin_amdgcn_readlane(pwin, pg - pw0), kbase, vbase, ok_cur);
+    for (int part = 0; part < 3; ++part) issue_part(0, cu, part, kbase, vbase);
+  }
+  int si = 0;                // ring slot of the tile being computed
+  long long remaining = n;   // tiles left in this worker's range
+  for (;;) {
+    const int t_first = cu.t;
+    const int t_end = static_cast<int>(min(static_cast<long long>(cu.tu), t_first + remaining));
+    const bool has_next = remaining > t_end - t_first;
+    Cursor nu = cu;
+    int pwin_n = 0;
+    if (has_next) {
+      nu = next_unit(cu);
+      pwin_n = load_window(nu.b, 0);
       if constexpr (kPrefetchQ) {
+        const bf16_t *qrow = q_row(nu, 0);
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) qf[0][ks] = qn[0][ks];
-      } else {
-        load_q(cc, qf);
+        for (int ks = 0; ks < KS; ++ks)
+          qn[0][ks] = *reinterpret_cast<const u32x4 *>(qrow + 32 * ks + 8 * lg);
       }
     }
-    const uint8_t *slot = ring + (k & 1) * G::SLOT;
-    u32x4 kf[2][KS], vf[DT];
+    reset();
+    for (int t = t_first; t < t_end; ++t) {
+      wait_vmcnt<0>();  // tile t, and every window and Q load issued before it
+      const uint8_t *slot = ring + si * G::SLOT;
+      u32x4 kf[2][KS], vf[DT];
 #pragma unroll
-    for (int e = 0; e < 2; ++e)
+      for (int e = 0; e < 2; ++e)
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
-        kf[e][ks] = *reinterpret_cast<const u32x4 *>(slot + (e * KS + ks) * kFragBytes + 16 * lane);
-    const bool prefix_tile = cc.t < 2 * cc.np;
-    int cap[NQ];
-    int limit;
-    bool full;
-    if (prefix_tile) {
-      limit = ok_cur ? min(32, cc.s - 32 * cc.t) : 0;
-      full = limit >= 32;
-#pragma unroll
-      for (int qt = 0; qt < NQ; ++qt) cap[qt] = 0x7fffffff;
-    } else {
-      const int u = cc.t - 2 * cc.np;
-      limit = p.w - 32 * u;
-      full = false;
-#pragma unroll
-      for (int qt = 0; qt < NQ; ++qt) cap[qt] = cap_blk[qt] - 32 * u;
-    }
-    // Every LDS read of the previous iteration (from the slot refilled
-    // below) and this tile's key fragments have completed.
-    __builtin_amdgcn_s_waitcnt(0xF | (0x3 << 14) | (0x7 << 4));  // lgkmcnt(0)
-    // The value fragments are read from LDS only before the P.V product, so
-    // they and the key fragments are never live together.
-    auto read_values = [&]() {
+        for (int ks = 0; ks < KS; ++ks)
+          kf[e][ks] = *reinterpret_cast<const u32x4 *>(slot + (e * KS + ks) * kFragBytes + 16 * lane);
+      const bool prefix_tile = t < 2 * cu.np;
+      int cap[NQ];
+      int limit;
+      bool full;
       if (prefix_tile) {
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt)
           vf[dt] = *reinterpret_cast<const u32x4 *>(slot + (2 * KS + dt) * kFragBytes + 16 * lane);
+        limit = ok_cur ? min(32, cu.s - 32 * t) : 0;
+        full = limit >= 32;
         if (!full) {
           // invisible tokens enter P.V with probability 0; their values are
           // zeroed so whatever the page holds there (NaN, Inf) adds nothing
@@ -379,8 +408,11 @@ void attn_balanced_kernel(AttnParams p) {
 #pragma unroll
           for (int dt = 0; dt < DT; ++dt) vf[dt] &= keep;
         }
+#pragma unroll
+        for (int qt = 0; qt < NQ; ++qt) cap[qt] = 0x7fffffff;
       } else {
         // block values are token-major [32][DH] in the slot: gather V^T
+        const int ub = t - 2 * cu.np;
         const uint16_t *raw = reinterpret_cast<const uint16_t *>(slot + 2 * KS * kFragBytes);
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
@@ -389,33 +421,62 @@ void attn_balanced_kernel(AttnParams p) {
           for (int jj = 0; jj < 8; ++jj) v8[jj] = raw[(8 * lg + jj) * DH + 16 * dt + ln];
           vf[dt] = __builtin_bit_cast(u32x4, v8);
         }
+        limit = p.w - 32 * ub;
+        full = false;
+#pragma unroll
+        for (int qt = 0; qt < NQ; ++qt) cap[qt] = cap_blk[qt] - 32 * ub;
       }
-    };
+      // the slot's fragments are in registers before the other slot is
+      // refilled, and the refill below completes the previous reads
+      __builtin_amdgcn_s_waitcnt(0xF | (0x3 << 14) | (0x7 << 4));  // lgkmcnt(0)
 
-    // tile k + 1 (= ci) goes to the other slot; its page id arrived with tile k
-    const bool refill = k + 1 < n;
-    if (refill) {
-      tile_src(ci, __builtin_amdgcn_readfirstlane(pid_next), kbase, vbase, ok_next);
-      if constexpr (kPrefetchQ)
-        if (ci.t == 0) load_q(ci, qn);  // tile k + 1 opens a unit
+      // the next tile: this unit's t + 1, or the next unit's first tile
+      const bool in_unit = t + 1 < t_end;
+      const bool refill = in_unit || has_next;
+      Cursor ci = in_unit ? cu : nu;
+      ci.t = in_unit ? t + 1 : 0;
+      ci = uniform(ci);
+      if (refill) {
+        int page = 0;
+        if (ci.t < 2 * ci.np) {
+          const int pg = ci.t >> 1;
+          if (!in_unit) {
+            page = __builtin_amdgcn_readlane(pwin_n, pg);
+          } else {
+            if (pg - pw0 >= 64) {  // the next window of this unit
+              pwin = pwin_x;
+              pw0 = x_pw0;
+              x_pw0 = -1;
+            }
+            page = __builtin_amdgcn_readlane(pwin, pg - pw0);
+            // first issue in a window: load the one after it
+            if (x_pw0 < 0 && pw0 + 64 < cu.np) {
+              x_pw0 = pw0 + 64;
+              pwin_x = load_window(cu.b, x_pw0);
+            }
+          }
+        }
+        tile_src(ci, page, kbase, vbase, ok_cur);  // ok_cur now describes tile t + 1
+      }
+      const int sn = si ^ 1;
+      compute_tile<DH, NQ>(st, kf, vf, qf, cap, limit, full, p.scale_log2, lg, [&](int part) {
+        if (refill) issue_part(sn, ci, part, kbase, vbase);
+      });
+      si = sn;
     }
-    Cursor cn = ci;  // tile k + 2
-    advance(cn);
-    if (k + 2 < n) pid_next = load_pid(cn);
-    const int si = (k + 1) & 1;
-    compute_tile<DH, NQ>(st, kf, vf, qf, cap, limit, full, p.scale_log2, lg, [&](int part) {
-      if (refill) issue_part(si, ci, part, kbase, vbase);
-      if (part == 2) read_values();
-    });
-    const bool unit_end = cc.t == cc.tu - 1;
-    if (unit_end || k + 1 == n) {
-      flush(cc, started_here && unit_end);
-      started_here = true;  // every later unit starts inside this worker
-      reset();
+    flush(cu, t_first == 0 && t_end == cu.tu);
+    remaining -= t_end - t_first;
+    if (remaining <= 0) break;
+    cu = nu;
+    pwin = pwin_n;
+    pw0 = 0;
+    x_pw0 = -1;
+    if constexpr (kPrefetchQ) {
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) qf[0][ks] = qn[0][ks];
+    } else {
+      load_q(cu, qf);
     }
-    cc = uniform(ci);
-    ci = uniform(cn);
-    ok_cur = ok_next;
   }
 }
 
