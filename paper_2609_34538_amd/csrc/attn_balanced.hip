@@ -359,6 +359,7 @@ void attn_balanced_kernel(AttnParams p) {
     tile_src(cu, __builtin_amdgcn_readlane(pwin, pg - pw0), kbase, vbase, ok_cur);
     for (int part = 0; part < 3; ++part) issue_part(0, cu, part, kbase, vbase);
   }
+  long long g_unit = g0 - c0.t;  // global index of the current unit's first tile
   int si = 0;                // ring slot of the tile being computed
   long long remaining = n;   // tiles left in this worker's range
   for (;;) {
@@ -465,6 +466,15 @@ void attn_balanced_kernel(AttnParams p) {
       si = sn;
     }
     flush(cu, t_first == 0 && t_end == cu.tu);
+    if (t_first == 0 && lane == 0) {
+      // this worker holds the unit's first tile: record where the unit's
+      // pieces start and how many workers share it, for the merge
+      const long long jl = worker_of(g_unit + cu.tu - 1, T, W);
+      const int unit = cu.b * p.hkv + cu.kvh;
+      p.ws_rec[2 * unit] = unit + j;
+      p.ws_rec[2 * unit + 1] = static_cast<int>(jl - j + 1);
+    }
+    g_unit += cu.tu;
     remaining -= t_end - t_first;
     if (remaining <= 0) break;
     cu = nu;
@@ -481,80 +491,75 @@ void attn_balanced_kernel(AttnParams p) {
 }
 
 // Merge of a unit's pieces (as the chunked kernel's merge, over the pieces
-// u + j of the workers j that share unit u). One single-wave workgroup per
-// (unit, 8 rows, 32 columns); units held by one worker exit at once.
-constexpr int kRowsPerBlock = 8;
-constexpr int kColsPerBlock = 32;
+// of the workers that share the unit): one 256-thread workgroup per unit,
+// one thread per (row, 4 columns) item; the unit's first piece and piece
+// count come from the record its first worker wrote, and units held whole
+// by one worker exit at once.
+constexpr int kMergeThreads = 256;
 constexpr int kEager = 8;
 
 template <typename T, int DH>
-__global__ __launch_bounds__(64) void attn_balanced_combine_kernel(AttnParams p) {
-  const int lane = threadIdx.x;
-  const TileMap tm = tile_map(p, lane, false);
+__global__ __launch_bounds__(kMergeThreads) void attn_balanced_combine_kernel(AttnParams p) {
   const int unit = blockIdx.x;  // b * hkv + kvh
+  const int piece0 = p.ws_rec[2 * unit];
+  const int np = p.ws_rec[2 * unit + 1];
+  if (np <= 1) return;  // written by its worker
   const int b = unit / p.hkv, kvh = unit % p.hkv;
-  const int tu = __builtin_amdgcn_readlane(tm.tu, b);
-  const long long s_u = readlane64(tm.incl, b) - static_cast<long long>(tu) * (p.hkv - kvh);
-  const long long jf = worker_of(s_u, tm.total, tm.workers);
-  const long long jl = worker_of(s_u + tu - 1, tm.total, tm.workers);
-  if (jf == jl) return;  // written by its worker
-  const int np = static_cast<int>(jl - jf + 1);
-
-  const int row = blockIdx.y * kRowsPerBlock + lane / 8;
-  const int c = blockIdx.z * kColsPerBlock + 4 * (lane % 8);
-  if (row >= p.rows || c >= DH) return;
-  const size_t piece0 = static_cast<size_t>(unit) + jf;
-  const float *mrow = p.ws_m + static_cast<size_t>(row) * p.piece_cap + piece0;
-  const float *lrow = p.ws_l + static_cast<size_t>(row) * p.piece_cap + piece0;
-  const float *orow = p.ws_o + (piece0 * p.rows + row) * DH + c;
+  constexpr int CG = DH / 4;  // column groups of a row
   const size_t ostride = static_cast<size_t>(p.rows) * DH;
-
-  float mv[kEager], lv[kEager];
-  float4 ov[kEager];
+  for (int item = threadIdx.x; item < p.rows * CG; item += kMergeThreads) {
+    const int row = item / CG;
+    const int c = 4 * (item % CG);
+    const float *mrow = p.ws_m + static_cast<size_t>(row) * p.piece_cap + piece0;
+    const float *lrow = p.ws_l + static_cast<size_t>(row) * p.piece_cap + piece0;
+    const float *orow = p.ws_o + (static_cast<size_t>(piece0) * p.rows + row) * DH + c;
+    float mv[kEager], lv[kEager];
+    float4 ov[kEager];
 #pragma unroll
-  for (int k = 0; k < kEager; ++k) {
-    const int kk = k < np ? k : 0;  // pieces past the count re-read the first
-    mv[k] = mrow[kk];
-    lv[k] = lrow[kk];
-    ov[k] = *reinterpret_cast<const float4 *>(orow + kk * ostride);
-  }
-  float mx = -__builtin_huge_valf();
-#pragma unroll
-  for (int k = 0; k < kEager; ++k) mx = k < np ? fmaxf(mx, mv[k]) : mx;
-  float den = 0.f, n0 = 0.f, n1 = 0.f, n2 = 0.f, n3 = 0.f;
-#pragma unroll
-  for (int k = 0; k < kEager; ++k) {
-    if (k < np) {
-      const float sc = exp2f(mv[k] - mx);
-      den += sc * lv[k];
-      n0 += sc * ov[k].x;
-      n1 += sc * ov[k].y;
-      n2 += sc * ov[k].z;
-      n3 += sc * ov[k].w;
+    for (int k = 0; k < kEager; ++k) {
+      const int kk = k < np ? k : 0;  // pieces past the count re-read the first
+      mv[k] = mrow[kk];
+      lv[k] = lrow[kk];
+      ov[k] = *reinterpret_cast<const float4 *>(orow + kk * ostride);
     }
+    float mx = -__builtin_huge_valf();
+#pragma unroll
+    for (int k = 0; k < kEager; ++k) mx = k < np ? fmaxf(mx, mv[k]) : mx;
+    float den = 0.f, n0 = 0.f, n1 = 0.f, n2 = 0.f, n3 = 0.f;
+#pragma unroll
+    for (int k = 0; k < kEager; ++k) {
+      if (k < np) {
+        const float sc = exp2f(mv[k] - mx);
+        den += sc * lv[k];
+        n0 += sc * ov[k].x;
+        n1 += sc * ov[k].y;
+        n2 += sc * ov[k].z;
+        n3 += sc * ov[k].w;
+      }
+    }
+    for (int k = kEager; k < np; ++k) {
+      const float m = mrow[k], l = lrow[k];
+      const float4 o = *reinterpret_cast<const float4 *>(orow + k * ostride);
+      const float nm = fmaxf(mx, m);
+      const float a = exp2f(mx - nm), sc = exp2f(m - nm);
+      den = den * a + sc * l;
+      n0 = n0 * a + sc * o.x;
+      n1 = n1 * a + sc * o.y;
+      n2 = n2 * a + sc * o.z;
+      n3 = n3 * a + sc * o.w;
+      mx = nm;
+    }
+    const int i = row / p.group, h = kvh * p.group + row % p.group;
+    T *out = static_cast<T *>(p.out) + ((static_cast<size_t>(b) * p.w + i) * p.hq + h) * DH + c;
+    const float inv = 1.f / den;
+    out[0] = from_f32<T>(n0 * inv);
+    out[1] = from_f32<T>(n1 * inv);
+    out[2] = from_f32<T>(n2 * inv);
+    out[3] = from_f32<T>(n3 * inv);
+    if (p.lse && c == 0)
+      p.lse[(static_cast<size_t>(b) * p.hq + h) * p.w + i] =
+          (mx + log2f(den)) * 0.69314718055994530942f;
   }
-  for (int k = kEager; k < np; ++k) {
-    const float m = mrow[k], l = lrow[k];
-    const float4 o = *reinterpret_cast<const float4 *>(orow + k * ostride);
-    const float nm = fmaxf(mx, m);
-    const float a = exp2f(mx - nm), sc = exp2f(m - nm);
-    den = den * a + sc * l;
-    n0 = n0 * a + sc * o.x;
-    n1 = n1 * a + sc * o.y;
-    n2 = n2 * a + sc * o.z;
-    n3 = n3 * a + sc * o.w;
-    mx = nm;
-  }
-  const int i = row / p.group, h = kvh * p.group + row % p.group;
-  T *out = static_cast<T *>(p.out) + ((static_cast<size_t>(b) * p.w + i) * p.hq + h) * DH + c;
-  const float inv = 1.f / den;
-  out[0] = from_f32<T>(n0 * inv);
-  out[1] = from_f32<T>(n1 * inv);
-  out[2] = from_f32<T>(n2 * inv);
-  out[3] = from_f32<T>(n3 * inv);
-  if (p.lse && c == 0)
-    p.lse[(static_cast<size_t>(b) * p.hq + h) * p.w + i] =
-        (mx + log2f(den)) * 0.69314718055994530942f;
 }
 
 // Blocks of up to 16 query rows: one row tile per wave; 17..32 rows: two
@@ -571,9 +576,8 @@ hipError_t launch_dh(const AttnParams &p, hipStream_t s) {
 
 template <int DH>
 hipError_t launch_combine_dh(const AttnParams &p, hipStream_t s) {
-  const dim3 grid(p.batch * p.hkv, (p.rows + kRowsPerBlock - 1) / kRowsPerBlock,
-                  (DH + kColsPerBlock - 1) / kColsPerBlock);
-  return launch_kernel(attn_balanced_combine_kernel<bf16_t, DH>, grid, dim3(64), s, p);
+  return launch_kernel(attn_balanced_combine_kernel<bf16_t, DH>, dim3(p.batch * p.hkv),
+                       dim3(kMergeThreads), s, p);
 }
 
 }  // namespace

@@ -75,7 +75,7 @@ struct Plan {
   int nsplit_ml;        // nsplit rounded up to a multiple of 4
   int n_workers;        // balanced schedule: workers launched
   int piece_cap;        // balanced schedule: pieces the workspace holds
-  size_t ws_o_bytes, ws_ml_bytes, total;
+  size_t ws_o_bytes, ws_ml_bytes, ws_rec_bytes, total;
 };
 
 // Prefix pages of one sequence are cut into splits of pages_per_split pages;
@@ -112,7 +112,9 @@ das_status make_plan(const das_cache *c, const das_batch *b, int hq, int w,
     const size_t pieces = static_cast<size_t>(plan->piece_cap);
     plan->ws_o_bytes = align_up(pieces * plan->rows * c->head_dim * sizeof(float));
     plan->ws_ml_bytes = align_up(pieces * plan->rows * sizeof(float));
-    plan->total = plan->ws_o_bytes + 2 * plan->ws_ml_bytes;
+    plan->ws_rec_bytes =
+        align_up(static_cast<size_t>(b->batch) * c->num_kv_heads * 2 * sizeof(int32_t));
+    plan->total = plan->ws_o_bytes + 2 * plan->ws_ml_bytes + plan->ws_rec_bytes;
     // merge grid: (sequence, KV head) x 64 threads along x
     if (static_cast<long long>(b->batch) * c->num_kv_heads * 64 > 0xffffffffLL)
       return DAS_ERR_SHAPE;
@@ -120,6 +122,7 @@ das_status make_plan(const das_cache *c, const das_batch *b, int hq, int w,
   }
   plan->n_workers = 0;
   plan->piece_cap = 0;
+  plan->ws_rec_bytes = 0;
   const int maxp = b->max_pages_per_seq;
   int pps = o ? o->pages_per_split : 0;
   if (pps == 0) {
@@ -213,6 +216,7 @@ das_status prepare_attn(const das_cache *c, const das_batch *b, int layer, int k
   p.block_table = b->block_table;
   p.dev_error = b->dev_error;
   p.ws_o = p.ws_m = p.ws_l = nullptr;
+  p.ws_rec = nullptr;
   p.batch = b->batch;
   p.hq = hq;
   p.hkv = c->num_kv_heads;
@@ -241,6 +245,7 @@ das_status launch_attn(AttnParams p, const Plan &plan, int dtype, int dh, void *
   p.ws_o = reinterpret_cast<float *>(wsb);
   p.ws_m = reinterpret_cast<float *>(wsb + plan.ws_o_bytes);
   p.ws_l = reinterpret_cast<float *>(wsb + plan.ws_o_bytes + plan.ws_ml_bytes);
+  p.ws_rec = reinterpret_cast<int32_t *>(wsb + plan.ws_o_bytes + 2 * plan.ws_ml_bytes);
   if (plan.path == DAS_PATH_BALANCED)
     return launch_attn_balanced(p, dh, stream) == hipSuccess ? DAS_OK : DAS_ERR_HIP;
   const bool mfma = plan.path == DAS_PATH_MFMA;

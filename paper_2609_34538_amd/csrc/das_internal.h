@@ -38,6 +38,7 @@ struct AttnParams {
   // each) and the piece capacity of the workspace (ws_o [piece_cap][rows][dh],
   // ws_m / ws_l [rows][piece_cap])
   int32_t n_workers, piece_cap;
+  int32_t *ws_rec;       // balanced schedule: per unit {first piece, piece count}
 };
 
 struct AppendParams {

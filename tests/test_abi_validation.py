@@ -273,11 +273,15 @@ def test_balanced_schedule_workspace_and_limits():
     al = lambda x: (x + 255) // 256 * 256
     c, b = make_cache(hkv=8, dh=96), make_batch(B=4, maxp=10)
     rows = 16 * 2  # w 16, G 2
+    # plus a {first piece, piece count} record per (sequence, KV head)
     pieces = 4 * 8 + 256 * 6
-    assert ws_bytes(c, b, hq=16, w=16, opts=o) == al(pieces * rows * 96 * 4) + 2 * al(pieces * rows * 4)
+    rec = al(4 * 8 * 8)
+    assert ws_bytes(c, b, hq=16, w=16, opts=o) == \
+        al(pieces * rows * 96 * 4) + 2 * al(pieces * rows * 4) + rec
     c128 = make_cache(hkv=8, dh=128)
     pieces = 4 * 8 + 256 * 5
-    assert ws_bytes(c128, b, hq=8, w=16, opts=o) == al(pieces * 16 * 128 * 4) + 2 * al(pieces * 16 * 4)
+    assert ws_bytes(c128, b, hq=8, w=16, opts=o) == \
+        al(pieces * 16 * 128 * 4) + 2 * al(pieces * 16 * 4) + rec
     # limits: 64 sequences, 32 query rows (16 at head dim 128)
     assert ws_bytes(c, make_batch(B=64, maxp=10), hq=8, w=32, opts=o) > 0
     assert ws_bytes(c, make_batch(B=65, maxp=10), hq=8, w=32, opts=o) == 0
