@@ -492,54 +492,73 @@ void attn_balanced_kernel(AttnParams p) {
 
 // Merge of a unit's pieces (as the chunked kernel's merge, over the pieces
 // of the workers that share the unit): one 256-thread workgroup per unit,
-// one thread per (row, 4 columns) item; the unit's first piece and piece
-// count come from the record its first worker wrote, and units held whole
-// by one worker exit at once.
+// each thread holding IT (row, 4 columns) items and issuing the loads of all
+// of them at once, so the merge costs two memory round trips (the record,
+// then the pieces) whatever the block width, and a unit held whole by one
+// worker occupies four waves for one round trip only. The unit's first piece
+// and piece count come from the record its first worker wrote.
 constexpr int kMergeThreads = 256;
-constexpr int kEager = 8;
+constexpr int kEager = 4;  // pieces per item loaded at once (units rarely have more)
 
-template <typename T, int DH>
+template <int DH>
+constexpr int merge_items(int rows) {
+  return (rows * (DH / 4) + kMergeThreads - 1) / kMergeThreads;
+}
+static_assert(merge_items<64>(32) == 2 && merge_items<96>(32) == 3 && merge_items<128>(16) == 2,
+              "items per merge thread at the largest balanced blocks");
+
+template <typename T, int DH, int IT>
 __global__ __launch_bounds__(kMergeThreads) void attn_balanced_combine_kernel(AttnParams p) {
   const int unit = blockIdx.x;  // b * hkv + kvh
   const int piece0 = p.ws_rec[2 * unit];
   const int np = p.ws_rec[2 * unit + 1];
   if (np <= 1) return;  // written by its worker
-  const int b = unit / p.hkv, kvh = unit % p.hkv;
   constexpr int CG = DH / 4;  // column groups of a row
+  const int n_items = p.rows * CG;
+  const int b = unit / p.hkv, kvh = unit % p.hkv;
   const size_t ostride = static_cast<size_t>(p.rows) * DH;
-  for (int item = threadIdx.x; item < p.rows * CG; item += kMergeThreads) {
-    const int row = item / CG;
-    const int c = 4 * (item % CG);
-    const float *mrow = p.ws_m + static_cast<size_t>(row) * p.piece_cap + piece0;
-    const float *lrow = p.ws_l + static_cast<size_t>(row) * p.piece_cap + piece0;
-    const float *orow = p.ws_o + (static_cast<size_t>(piece0) * p.rows + row) * DH + c;
-    float mv[kEager], lv[kEager];
-    float4 ov[kEager];
+  const float *mrow[IT], *lrow[IT], *orow[IT];
+  float mv[IT][kEager], lv[IT][kEager];
+  float4 ov[IT][kEager];
+#pragma unroll
+  for (int it = 0; it < IT; ++it) {
+    // items past the block's last repeat the first (computed, never stored)
+    const int item0 = threadIdx.x + it * kMergeThreads;
+    const int item = item0 < n_items ? item0 : 0;
+    const int row = item / CG, c = 4 * (item % CG);
+    mrow[it] = p.ws_m + static_cast<size_t>(row) * p.piece_cap + piece0;
+    lrow[it] = p.ws_l + static_cast<size_t>(row) * p.piece_cap + piece0;
+    orow[it] = p.ws_o + (static_cast<size_t>(piece0) * p.rows + row) * DH + c;
 #pragma unroll
     for (int k = 0; k < kEager; ++k) {
-      const int kk = k < np ? k : 0;  // pieces past the count re-read the first
-      mv[k] = mrow[kk];
-      lv[k] = lrow[kk];
-      ov[k] = *reinterpret_cast<const float4 *>(orow + kk * ostride);
+      if (k < np) {  // uniform over the workgroup
+        mv[it][k] = mrow[it][k];
+        lv[it][k] = lrow[it][k];
+        ov[it][k] = *reinterpret_cast<const float4 *>(orow[it] + k * ostride);
+      }
     }
+  }
+#pragma unroll
+  for (int it = 0; it < IT; ++it) {
+    const int item = threadIdx.x + it * kMergeThreads;
     float mx = -__builtin_huge_valf();
 #pragma unroll
-    for (int k = 0; k < kEager; ++k) mx = k < np ? fmaxf(mx, mv[k]) : mx;
+    for (int k = 0; k < kEager; ++k) mx = k < np ? fmaxf(mx, mv[it][k]) : mx;
     float den = 0.f, n0 = 0.f, n1 = 0.f, n2 = 0.f, n3 = 0.f;
 #pragma unroll
     for (int k = 0; k < kEager; ++k) {
       if (k < np) {
-        const float sc = exp2f(mv[k] - mx);
-        den += sc * lv[k];
-        n0 += sc * ov[k].x;
-        n1 += sc * ov[k].y;
-        n2 += sc * ov[k].z;
-        n3 += sc * ov[k].w;
+        const float sc = exp2f(mv[it][k] - mx);
+        den += sc * lv[it][k];
+        n0 += sc * ov[it][k].x;
+        n1 += sc * ov[it][k].y;
+        n2 += sc * ov[it][k].z;
+        n3 += sc * ov[it][k].w;
       }
     }
     for (int k = kEager; k < np; ++k) {
-      const float m = mrow[k], l = lrow[k];
-      const float4 o = *reinterpret_cast<const float4 *>(orow + k * ostride);
+      const float m = mrow[it][k], l = lrow[it][k];
+      const float4 o = *reinterpret_cast<const float4 *>(orow[it] + k * ostride);
       const float nm = fmaxf(mx, m);
       const float a = exp2f(mx - nm), sc = exp2f(m - nm);
       den = den * a + sc * l;
@@ -549,6 +568,8 @@ __global__ __launch_bounds__(kMergeThreads) void attn_balanced_combine_kernel(At
       n3 = n3 * a + sc * o.w;
       mx = nm;
     }
+    if (item >= n_items) continue;
+    const int row = item / CG, c = 4 * (item % CG);
     const int i = row / p.group, h = kvh * p.group + row % p.group;
     T *out = static_cast<T *>(p.out) + ((static_cast<size_t>(b) * p.w + i) * p.hq + h) * DH + c;
     const float inv = 1.f / den;
@@ -576,8 +597,13 @@ hipError_t launch_dh(const AttnParams &p, hipStream_t s) {
 
 template <int DH>
 hipError_t launch_combine_dh(const AttnParams &p, hipStream_t s) {
-  return launch_kernel(attn_balanced_combine_kernel<bf16_t, DH>, dim3(p.batch * p.hkv),
-                       dim3(kMergeThreads), s, p);
+  const dim3 grid(static_cast<unsigned>(p.batch * p.hkv)), block(kMergeThreads);
+  switch (merge_items<DH>(p.rows)) {
+    case 1: return launch_kernel(attn_balanced_combine_kernel<bf16_t, DH, 1>, grid, block, s, p);
+    case 2: return launch_kernel(attn_balanced_combine_kernel<bf16_t, DH, 2>, grid, block, s, p);
+    case 3: return launch_kernel(attn_balanced_combine_kernel<bf16_t, DH, 3>, grid, block, s, p);
+    default: return hipErrorInvalidValue;  // more rows than the balanced path takes
+  }
 }
 
 }  // namespace

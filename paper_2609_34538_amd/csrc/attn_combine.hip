@@ -14,13 +14,13 @@ namespace {
 
 constexpr int kRowsPerBlock = 8;
 constexpr int kColsPerBlock = 32;
-constexpr int kEager = 16;  // splits whose partials are loaded before the count is known
+constexpr int kEager = 24;  // splits whose partials are loaded before the count is known
 
 // One single-wave workgroup per (sequence, KV head, 8 rows, 32 columns); one
 // thread per (row, 4 consecutive columns). A row's per-split maxima and sums
 // are contiguous, so they arrive as 16-byte vectors; the partials of the first
-// 16 splits the workspace holds are loaded together with the prefix length,
-// so a merge of up to 16 splits costs one memory round trip. Values of splits
+// 24 splits the workspace holds are loaded together with the prefix length,
+// so a merge of up to 24 splits costs one memory round trip. Values of splits
 // past the sequence's count are discarded by selection, never used in
 // arithmetic.
 template <typename T, int DH>
@@ -40,18 +40,20 @@ __global__ __launch_bounds__(64) void attn_combine_kernel(AttnParams p, int skip
   float4 ov[kEager];
 #pragma unroll
   for (int k4 = 0; k4 < kEager / 4; ++k4) {
-    // groups past the row's nsplit_ml (a multiple of 4) re-read its last group;
-    // those splits are beyond the count and discarded below
-    const int g4 = min(4 * k4, p.nsplit_ml - 4);
-    const float4 m4 = *reinterpret_cast<const float4 *>(p.ws_m + mbase + g4);
-    const float4 l4 = *reinterpret_cast<const float4 *>(p.ws_l + mbase + g4);
-    mv[4 * k4] = m4.x, mv[4 * k4 + 1] = m4.y, mv[4 * k4 + 2] = m4.z, mv[4 * k4 + 3] = m4.w;
-    lv[4 * k4] = l4.x, lv[4 * k4 + 1] = l4.y, lv[4 * k4 + 2] = l4.z, lv[4 * k4 + 3] = l4.w;
+    // the row's nsplit_ml (a multiple of 4) slots; split slots past the
+    // plan's count are not loaded (a uniform branch), those past the
+    // sequence's count are discarded below
+    if (4 * k4 < p.nsplit_ml) {
+      const float4 m4 = *reinterpret_cast<const float4 *>(p.ws_m + mbase + 4 * k4);
+      const float4 l4 = *reinterpret_cast<const float4 *>(p.ws_l + mbase + 4 * k4);
+      mv[4 * k4] = m4.x, mv[4 * k4 + 1] = m4.y, mv[4 * k4 + 2] = m4.z, mv[4 * k4 + 3] = m4.w;
+      lv[4 * k4] = l4.x, lv[4 * k4 + 1] = l4.y, lv[4 * k4 + 2] = l4.z, lv[4 * k4 + 3] = l4.w;
+    }
   }
 #pragma unroll
   for (int k = 0; k < kEager; ++k) {
-    const size_t r = obase + static_cast<size_t>(k < p.nsplit ? k : 0) * p.rows;
-    ov[k] = *reinterpret_cast<const float4 *>(p.ws_o + r * DH + c0);
+    if (k < p.nsplit)
+      ov[k] = *reinterpret_cast<const float4 *>(p.ws_o + (obase + static_cast<size_t>(k) * p.rows) * DH + c0);
   }
   // keep every load above ahead of the first use of its result (one round trip)
   __builtin_amdgcn_sched_barrier(0);

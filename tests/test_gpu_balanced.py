@@ -31,7 +31,7 @@ def _run(lens, hq, hkv, dh, w, d=2, path="balanced", seed=0):
     return wl, cd, (cache, batch, q, kb, vb), out, lse
 
 
-@pytest.mark.parametrize("hkv,dh,w", [(1, 96, 32), (3, 128, 16), (2, 64, 7)])
+@pytest.mark.parametrize("hkv,dh,w", [(1, 96, 32), (3, 128, 16), (2, 64, 7), (1, 64, 32)])
 def test_long_sequence_among_short_ones(hkv, dh, w):
     # the 40000-token unit spans dozens of workers: more pieces than the
     # merge loads at once
