@@ -20,8 +20,10 @@
 // tiles in flight (the chunked kernel's depth), 0.72-0.73 against 0.68-0.69
 // of 8 TB/s on the same box. At the end
 // of a unit (or of its range) the worker writes the unit's normalised output
-// when it processed the whole unit, otherwise an unnormalised piece
-// (m, l, O) that the merge kernel combines with the unit's other pieces.
+// when it processed the whole unit, otherwise a piece (the running maximum
+// m, the sum l and the normalised output O / l in fp16 under a per-row
+// power-of-two scale) that the merge kernel combines with the unit's other
+// pieces.
 // Pieces are indexed unit + worker: along the tile sequence either the unit
 // or the worker (or both) advances, so the index is unique, and a unit's
 // pieces are consecutive.
@@ -37,6 +39,8 @@ namespace das {
 namespace {
 
 constexpr int kMinTilesPerWorker = 16;  // fewer tiles per worker: fewer workers
+
+typedef _Float16 h16x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ long long readlane64(long long x, int lane) {
   const uint32_t lo = __builtin_amdgcn_readlane(static_cast<uint32_t>(x), lane);
@@ -293,14 +297,35 @@ void attn_balanced_kernel(AttnParams p) {
           p.lse[(static_cast<size_t>(x.b) * p.hq + h) * p.w + i] =
               (st.m[qt] + log2f(st.l[qt])) * 0.69314718055994530942f;
       } else {
-        float *orow = p.ws_o + (piece * p.rows + row) * DH;
+        // Piece record (one worker's, 256-byte aligned, so its lines are
+        // written by this wave alone): the row's normalised output O / l in
+        // fp16, scaled by 2^-e so that its largest magnitude lies in
+        // [2^14, 2^15), then {m, l, q = l 2^e, 0}; the merge takes the
+        // row's unnormalised output as the stored values times q. Half the
+        // bytes of fp32 partials: the stores of a piece written in the
+        // middle of a worker's range delay its next tile waits.
+        uint8_t *rec = reinterpret_cast<uint8_t *>(p.ws_o) + piece * p.piece_stride;
+        const float inv = st.l[qt] > 0.f ? 1.f / st.l[qt] : 0.f;
+        float amax = 0.f;
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt)
-          *reinterpret_cast<f32x4 *>(orow + 16 * dt + 4 * lg) = st.o[qt][dt];
+#pragma unroll
+          for (int v = 0; v < 4; ++v) amax = fmaxf(amax, fabsf(st.o[qt][dt][v]));
+        amax = group_max(amax) * inv;  // the 4 lanes of a row share its skip test
+        const int e = (amax > 0.f && amax <= 3.4e38f) ? __builtin_amdgcn_frexp_expf(amax) - 15 : 0;
+        const float sc = __builtin_amdgcn_ldexpf(inv, -e);
+        _Float16 *orow = reinterpret_cast<_Float16 *>(rec) + row * DH;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+          const f32x4 o = st.o[qt][dt];
+          const h16x4 hv = {static_cast<_Float16>(o[0] * sc), static_cast<_Float16>(o[1] * sc),
+                            static_cast<_Float16>(o[2] * sc), static_cast<_Float16>(o[3] * sc)};
+          *reinterpret_cast<h16x4 *>(orow + 16 * dt + 4 * lg) = hv;
+        }
         if (lg == 0) {
-          // -inf when no position was visible: weight 0 in the merge
-          p.ws_m[static_cast<size_t>(row) * p.piece_cap + piece] = st.m[qt];
-          p.ws_l[static_cast<size_t>(row) * p.piece_cap + piece] = st.l[qt];
+          // m = -inf and l = 0 when no position was visible: weight 0 in the merge
+          const f32x4 meta = {st.m[qt], st.l[qt], __builtin_amdgcn_ldexpf(st.l[qt], e), 0.f};
+          *reinterpret_cast<f32x4 *>(rec + p.rows * DH * 2 + row * 16) = meta;
         }
       }
     }
@@ -516,56 +541,58 @@ __global__ __launch_bounds__(kMergeThreads) void attn_balanced_combine_kernel(At
   constexpr int CG = DH / 4;  // column groups of a row
   const int n_items = p.rows * CG;
   const int b = unit / p.hkv, kvh = unit % p.hkv;
-  const size_t ostride = static_cast<size_t>(p.rows) * DH;
-  const float *mrow[IT], *lrow[IT], *orow[IT];
-  float mv[IT][kEager], lv[IT][kEager];
-  float4 ov[IT][kEager];
+  const size_t stride = static_cast<size_t>(p.piece_stride);
+  const uint8_t *rec0 = reinterpret_cast<const uint8_t *>(p.ws_o) + piece0 * stride;
+  const uint8_t *orow[IT], *mrow[IT];
+  f32x4 meta[IT][kEager];
+  h16x4 ov[IT][kEager];
 #pragma unroll
   for (int it = 0; it < IT; ++it) {
     // items past the block's last repeat the first (computed, never stored)
     const int item0 = threadIdx.x + it * kMergeThreads;
     const int item = item0 < n_items ? item0 : 0;
     const int row = item / CG, c = 4 * (item % CG);
-    mrow[it] = p.ws_m + static_cast<size_t>(row) * p.piece_cap + piece0;
-    lrow[it] = p.ws_l + static_cast<size_t>(row) * p.piece_cap + piece0;
-    orow[it] = p.ws_o + (static_cast<size_t>(piece0) * p.rows + row) * DH + c;
+    orow[it] = rec0 + (row * DH + c) * 2;
+    mrow[it] = rec0 + p.rows * DH * 2 + row * 16;
 #pragma unroll
     for (int k = 0; k < kEager; ++k) {
       if (k < np) {  // uniform over the workgroup
-        mv[it][k] = mrow[it][k];
-        lv[it][k] = lrow[it][k];
-        ov[it][k] = *reinterpret_cast<const float4 *>(orow[it] + k * ostride);
+        meta[it][k] = *reinterpret_cast<const f32x4 *>(mrow[it] + k * stride);
+        ov[it][k] = *reinterpret_cast<const h16x4 *>(orow[it] + k * stride);
       }
     }
   }
 #pragma unroll
   for (int it = 0; it < IT; ++it) {
     const int item = threadIdx.x + it * kMergeThreads;
+    // piece k: maximum meta[0], sum meta[1], unnormalised output = stored * meta[2]
     float mx = -__builtin_huge_valf();
 #pragma unroll
-    for (int k = 0; k < kEager; ++k) mx = k < np ? fmaxf(mx, mv[it][k]) : mx;
+    for (int k = 0; k < kEager; ++k) mx = k < np ? fmaxf(mx, meta[it][k][0]) : mx;
     float den = 0.f, n0 = 0.f, n1 = 0.f, n2 = 0.f, n3 = 0.f;
 #pragma unroll
     for (int k = 0; k < kEager; ++k) {
       if (k < np) {
-        const float sc = exp2f(mv[it][k] - mx);
-        den += sc * lv[it][k];
-        n0 += sc * ov[it][k].x;
-        n1 += sc * ov[it][k].y;
-        n2 += sc * ov[it][k].z;
-        n3 += sc * ov[it][k].w;
+        const float sc = exp2f(meta[it][k][0] - mx);
+        const float w = sc * meta[it][k][2];
+        den += sc * meta[it][k][1];
+        n0 += w * static_cast<float>(ov[it][k][0]);
+        n1 += w * static_cast<float>(ov[it][k][1]);
+        n2 += w * static_cast<float>(ov[it][k][2]);
+        n3 += w * static_cast<float>(ov[it][k][3]);
       }
     }
     for (int k = kEager; k < np; ++k) {
-      const float m = mrow[it][k], l = lrow[it][k];
-      const float4 o = *reinterpret_cast<const float4 *>(orow[it] + k * ostride);
-      const float nm = fmaxf(mx, m);
-      const float a = exp2f(mx - nm), sc = exp2f(m - nm);
-      den = den * a + sc * l;
-      n0 = n0 * a + sc * o.x;
-      n1 = n1 * a + sc * o.y;
-      n2 = n2 * a + sc * o.z;
-      n3 = n3 * a + sc * o.w;
+      const f32x4 mk = *reinterpret_cast<const f32x4 *>(mrow[it] + k * stride);
+      const h16x4 o = *reinterpret_cast<const h16x4 *>(orow[it] + k * stride);
+      const float nm = fmaxf(mx, mk[0]);
+      const float a = exp2f(mx - nm), sc = exp2f(mk[0] - nm);
+      const float w = sc * mk[2];
+      den = den * a + sc * mk[1];
+      n0 = n0 * a + w * static_cast<float>(o[0]);
+      n1 = n1 * a + w * static_cast<float>(o[1]);
+      n2 = n2 * a + w * static_cast<float>(o[2]);
+      n3 = n3 * a + w * static_cast<float>(o[3]);
       mx = nm;
     }
     if (item >= n_items) continue;

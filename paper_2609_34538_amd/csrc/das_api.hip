@@ -75,6 +75,7 @@ struct Plan {
   int nsplit_ml;        // nsplit rounded up to a multiple of 4
   int n_workers;        // balanced schedule: workers launched
   int piece_cap;        // balanced schedule: pieces the workspace holds
+  int piece_stride;     // balanced schedule: bytes of one piece record
   size_t ws_o_bytes, ws_ml_bytes, ws_rec_bytes, total;
 };
 
@@ -109,12 +110,15 @@ das_status make_plan(const das_cache *c, const das_batch *b, int hq, int w,
     plan->pages_per_split = 0;
     plan->nsplit = 0;
     plan->nsplit_ml = 0;
+    // a piece record: the rows' fp16 outputs, then 16 bytes per row
+    plan->piece_stride = static_cast<int>(
+        align_up(static_cast<size_t>(plan->rows) * (c->head_dim * 2 + 16)));
     const size_t pieces = static_cast<size_t>(plan->piece_cap);
-    plan->ws_o_bytes = align_up(pieces * plan->rows * c->head_dim * sizeof(float));
-    plan->ws_ml_bytes = align_up(pieces * plan->rows * sizeof(float));
+    plan->ws_o_bytes = pieces * plan->piece_stride;
+    plan->ws_ml_bytes = 0;
     plan->ws_rec_bytes =
         align_up(static_cast<size_t>(b->batch) * c->num_kv_heads * 2 * sizeof(int32_t));
-    plan->total = plan->ws_o_bytes + 2 * plan->ws_ml_bytes + plan->ws_rec_bytes;
+    plan->total = plan->ws_o_bytes + plan->ws_rec_bytes;
     // merge grid: (sequence, KV head) x 64 threads along x
     if (static_cast<long long>(b->batch) * c->num_kv_heads * 64 > 0xffffffffLL)
       return DAS_ERR_SHAPE;
@@ -122,6 +126,7 @@ das_status make_plan(const das_cache *c, const das_batch *b, int hq, int w,
   }
   plan->n_workers = 0;
   plan->piece_cap = 0;
+  plan->piece_stride = 0;
   plan->ws_rec_bytes = 0;
   const int maxp = b->max_pages_per_seq;
   int pps = o ? o->pages_per_split : 0;
@@ -230,6 +235,7 @@ das_status prepare_attn(const das_cache *c, const das_batch *b, int layer, int k
   p.nsplit_ml = plan->nsplit_ml;
   p.n_workers = plan->n_workers;
   p.piece_cap = plan->piece_cap;
+  p.piece_stride = plan->piece_stride;
   // log2(e) / sqrt(dh): logits are kept in base-2 units so exp2 can be used.
   const double log2e = 1.4426950408889634074;
   p.scale_log2 = static_cast<float>(log2e / __builtin_sqrt(static_cast<double>(dh)));

@@ -27,6 +27,7 @@ struct AttnParams {
   const int32_t *block_table;  // [B][max_pages]
   uint32_t *dev_error;         // or nullptr
   float *ws_o;           // [B][Hkv][nsplit][rows][dh]     unnormalised partial O
+                         // (balanced schedule: piece records, see piece_stride)
   float *ws_m;           // [B][Hkv][rows][nsplit_ml]      running max (log2 units)
   float *ws_l;           // [B][Hkv][rows][nsplit_ml]      running sum
   int32_t batch, hq, hkv, group, w, rows;  // rows = w * group
@@ -35,9 +36,10 @@ struct AttnParams {
   int32_t nsplit_ml;     // nsplit rounded up to a multiple of 4 (16-byte rows of m, l)
   float scale_log2;      // log2(e) / sqrt(dh): logits in base-2 units
   // balanced schedule only: workers launched (one single-wave workgroup
-  // each) and the piece capacity of the workspace (ws_o [piece_cap][rows][dh],
-  // ws_m / ws_l [rows][piece_cap])
-  int32_t n_workers, piece_cap;
+  // each), the piece capacity of the workspace and the bytes of one piece
+  // record at ws_o (the record: [rows][dh] fp16 scaled normalised output,
+  // then [rows] x {m, l, q, 0} fp32; records are 256-byte aligned)
+  int32_t n_workers, piece_cap, piece_stride;
   int32_t *ws_rec;       // balanced schedule: per unit {first piece, piece count}
 };
 
