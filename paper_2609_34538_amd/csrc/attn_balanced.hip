@@ -40,8 +40,6 @@ namespace {
 
 constexpr int kMinTilesPerWorker = 16;  // fewer tiles per worker: fewer workers
 
-typedef _Float16 h16x4 __attribute__((ext_vector_type(4)));
-
 __device__ __forceinline__ long long readlane64(long long x, int lane) {
   const uint32_t lo = __builtin_amdgcn_readlane(static_cast<uint32_t>(x), lane);
   const uint32_t hi = __builtin_amdgcn_readlane(static_cast<uint32_t>(x >> 32), lane);
@@ -297,36 +295,12 @@ void attn_balanced_kernel(AttnParams p) {
           p.lse[(static_cast<size_t>(x.b) * p.hq + h) * p.w + i] =
               (st.m[qt] + log2f(st.l[qt])) * 0.69314718055994530942f;
       } else {
-        // Piece record (one worker's, 256-byte aligned, so its lines are
-        // written by this wave alone): the row's normalised output O / l in
-        // fp16, scaled by 2^-e so that its largest magnitude lies in
-        // [2^14, 2^15), then {m, l, q = l 2^e, 0}; the merge takes the
-        // row's unnormalised output as the stored values times q. Half the
-        // bytes of fp32 partials: the stores of a piece written in the
-        // middle of a worker's range delay its next tile waits.
-        uint8_t *rec = reinterpret_cast<uint8_t *>(p.ws_o) + piece * p.piece_stride;
-        const float inv = st.l[qt] > 0.f ? 1.f / st.l[qt] : 0.f;
-        float amax = 0.f;
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-          for (int v = 0; v < 4; ++v) amax = fmaxf(amax, fabsf(st.o[qt][dt][v]));
-        amax = group_max(amax) * inv;  // the 4 lanes of a row share its skip test
-        const int e = (amax > 0.f && amax <= 3.4e38f) ? __builtin_amdgcn_frexp_expf(amax) - 15 : 0;
-        const float sc = __builtin_amdgcn_ldexpf(inv, -e);
-        _Float16 *orow = reinterpret_cast<_Float16 *>(rec) + row * DH;
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) {
-          const f32x4 o = st.o[qt][dt];
-          const h16x4 hv = {static_cast<_Float16>(o[0] * sc), static_cast<_Float16>(o[1] * sc),
-                            static_cast<_Float16>(o[2] * sc), static_cast<_Float16>(o[3] * sc)};
-          *reinterpret_cast<h16x4 *>(orow + 16 * dt + 4 * lg) = hv;
-        }
-        if (lg == 0) {
-          // m = -inf and l = 0 when no position was visible: weight 0 in the merge
-          const f32x4 meta = {st.m[qt], st.l[qt], __builtin_amdgcn_ldexpf(st.l[qt], e), 0.f};
-          *reinterpret_cast<f32x4 *>(rec + p.rows * DH * 2 + row * 16) = meta;
-        }
+        // a piece record of its own (256-byte aligned, so its lines are
+        // written by this wave alone), in half the bytes of fp32 partials:
+        // the stores of a piece written in the middle of a worker's range
+        // delay its next tile waits
+        write_piece_row<DH>(reinterpret_cast<uint8_t *>(p.ws_o) + piece * p.piece_stride, p.rows,
+                            row, lg, st.o[qt], st.m[qt], st.l[qt]);
       }
     }
   };

@@ -7,7 +7,7 @@
 // and the natural-log normaliser is (M + log2 sum_s 2^(m_s - M) l_s) * ln 2.
 // Split 0 always holds the block's diagonal, so M is finite.
 
-#include "das_internal.h"
+#include "mfma_tile.h"
 
 namespace das {
 namespace {
@@ -107,6 +107,88 @@ __global__ __launch_bounds__(64) void attn_combine_kernel(AttnParams p, int skip
     p.lse[(static_cast<size_t>(b) * p.hq + h) * p.w + i] = (mx + log2f(den)) * 0.69314718055994530942f;
 }
 
+// The same merge over the piece records of the matrix-core kernel (one per
+// (sequence, KV head, split), piece_record_bytes each): a row's per-split
+// {m, l, q} arrive as one 16-byte vector and its outputs as fp16 values
+// scaled by q; the records of the first 24 splits are loaded together with
+// the prefix length.
+template <int DH>
+__global__ __launch_bounds__(64) void attn_combine_records_kernel(AttnParams p, int skip_single) {
+  const int unit = blockIdx.x;  // b * hkv + kvh
+  const int b = unit / p.hkv;
+  const int kvh = unit % p.hkv;
+  const int row = blockIdx.y * kRowsPerBlock + threadIdx.x / 8;
+  const int c = blockIdx.z * kColsPerBlock + 4 * (threadIdx.x % 8);
+  const bool live = row < p.rows && c < DH;
+  const int r0 = live ? row : 0, c0 = live ? c : 0;
+  const size_t stride = static_cast<size_t>(p.piece_stride);
+  const uint8_t *rec0 = reinterpret_cast<const uint8_t *>(p.ws_o) +
+                        static_cast<size_t>(unit) * p.nsplit * stride;
+  const uint8_t *orow = rec0 + (r0 * DH + c0) * 2;
+  const uint8_t *mrow = rec0 + static_cast<size_t>(p.rows) * DH * 2 + r0 * 16;
+
+  const int s_raw = p.prefix_len[b];
+  f32x4 meta[kEager];
+  h16x4 ov[kEager];
+#pragma unroll
+  for (int k = 0; k < kEager; ++k) {
+    if (k < p.nsplit) {  // split slots of the plan (uniform); past the sequence's count: unused
+      meta[k] = *reinterpret_cast<const f32x4 *>(mrow + k * stride);
+      ov[k] = *reinterpret_cast<const h16x4 *>(orow + k * stride);
+    }
+  }
+  // keep every load above ahead of the first use of its result (one round trip)
+  __builtin_amdgcn_sched_barrier(0);
+  bool bad;
+  const int S = clamp_prefix(s_raw, p.max_pages, &bad);
+  const int npages = (S + kPage - 1) / kPage;
+  const int ns = splits_of(npages, p.pages_per_split);
+  const bool write = live && !(ns == 1 && skip_single);
+
+  // split k: maximum meta[0], sum meta[1], unnormalised output = stored * meta[2]
+  float mx = -__builtin_huge_valf();
+#pragma unroll
+  for (int k = 0; k < kEager; ++k) mx = k < ns ? fmaxf(mx, meta[k][0]) : mx;
+  float den = 0.f, n0 = 0.f, n1 = 0.f, n2 = 0.f, n3 = 0.f;
+#pragma unroll
+  for (int k = 0; k < kEager; ++k) {
+    if (k < ns) {
+      const float sc = exp2f(meta[k][0] - mx);
+      const float wgt = sc * meta[k][2];
+      den += sc * meta[k][1];
+      n0 += wgt * static_cast<float>(ov[k][0]);
+      n1 += wgt * static_cast<float>(ov[k][1]);
+      n2 += wgt * static_cast<float>(ov[k][2]);
+      n3 += wgt * static_cast<float>(ov[k][3]);
+    }
+  }
+  // splits beyond the first 24, merged in the same online form
+  for (int k = kEager; k < ns && live; ++k) {
+    const f32x4 mk = *reinterpret_cast<const f32x4 *>(mrow + k * stride);
+    const h16x4 o = *reinterpret_cast<const h16x4 *>(orow + k * stride);
+    const float nm = fmaxf(mx, mk[0]);
+    const float a = exp2f(mx - nm), sc = exp2f(mk[0] - nm);
+    const float wgt = sc * mk[2];
+    den = den * a + sc * mk[1];
+    n0 = n0 * a + wgt * static_cast<float>(o[0]);
+    n1 = n1 * a + wgt * static_cast<float>(o[1]);
+    n2 = n2 * a + wgt * static_cast<float>(o[2]);
+    n3 = n3 * a + wgt * static_cast<float>(o[3]);
+    mx = nm;
+  }
+  if (!write) return;
+  const int i = row / p.group, g = row % p.group;
+  const int h = kvh * p.group + g;
+  bf16_t *out = static_cast<bf16_t *>(p.out) + ((static_cast<size_t>(b) * p.w + i) * p.hq + h) * DH + c;
+  const float inv = 1.f / den;
+  out[0] = f32_to_bf16(n0 * inv);
+  out[1] = f32_to_bf16(n1 * inv);
+  out[2] = f32_to_bf16(n2 * inv);
+  out[3] = f32_to_bf16(n3 * inv);
+  if (p.lse && c == 0)
+    p.lse[(static_cast<size_t>(b) * p.hq + h) * p.w + i] = (mx + log2f(den)) * 0.69314718055994530942f;
+}
+
 template <typename T, int DH>
 hipError_t launch_typed(const AttnParams &p, int skip_single, hipStream_t s) {
   dim3 grid(p.batch * p.hkv, (p.rows + kRowsPerBlock - 1) / kRowsPerBlock,
@@ -114,7 +196,21 @@ hipError_t launch_typed(const AttnParams &p, int skip_single, hipStream_t s) {
   return launch_kernel(attn_combine_kernel<T, DH>, grid, dim3(64), s, p, skip_single);
 }
 
+template <int DH>
+hipError_t launch_records(const AttnParams &p, int skip_single, hipStream_t s) {
+  dim3 grid(p.batch * p.hkv, (p.rows + kRowsPerBlock - 1) / kRowsPerBlock,
+            (DH + kColsPerBlock - 1) / kColsPerBlock);
+  return launch_kernel(attn_combine_records_kernel<DH>, grid, dim3(64), s, p, skip_single);
+}
+
 }  // namespace
+
+hipError_t launch_attn_combine_records(const AttnParams &p, int dh, int skip_single,
+                                       hipStream_t s) {
+  if (dh == 64) return launch_records<64>(p, skip_single, s);
+  if (dh == 96) return launch_records<96>(p, skip_single, s);
+  return launch_records<128>(p, skip_single, s);
+}
 
 hipError_t launch_attn_combine(const AttnParams &p, int dtype, int dh, int skip_single,
                                hipStream_t s) {

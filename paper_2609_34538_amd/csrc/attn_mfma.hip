@@ -40,9 +40,9 @@
 // a 32-token tile of that page is one contiguous block. The draft block's
 // values are token-major; their V^T fragments are gathered from LDS.
 //
-// A chunk ends by writing its (m, l, O) partial to the workspace for the
-// combine kernel, or, when its sequence has a single split, the normalised
-// output. Query rows of a row tile: row = i * G + g (block position i,
+// A chunk ends by writing its piece record (m, l and O / l in fp16 under a
+// per-row power-of-two scale) to the workspace for the combine kernel, or,
+// when its sequence has a single split, the normalised output. Query rows of a row tile: row = i * G + g (block position i,
 // head kvh * G + g). Logits are scaled into base-2 units after the product,
 // inside the exponent's fused multiply-add.
 
@@ -370,7 +370,8 @@ void attn_mfma_kernel(AttnParams p, int n_rg, int n_chunks) {
   }
 
   // Chunk result. Lane holds head dims 16dt + 4g .. +3 of row n of tile qt.
-  const size_t prow0 = ((static_cast<size_t>(b) * p.hkv + kvh) * p.nsplit + split) * p.rows;
+  uint8_t *prec = reinterpret_cast<uint8_t *>(p.ws_o) +
+                  ((static_cast<size_t>(b) * p.hkv + kvh) * p.nsplit + split) * p.piece_stride;
 #pragma unroll
   for (int qt = 0; qt < NQ; ++qt) {
     const int row = rt * ROWS + qt * 16 + ln;
@@ -394,15 +395,7 @@ void attn_mfma_kernel(AttnParams p, int n_rg, int n_chunks) {
         p.lse[(static_cast<size_t>(b) * p.hq + h) * p.w + i] =
             (st.m[qt] + log2f(st.l[qt])) * 0.69314718055994530942f;
     } else {
-      float *orow = p.ws_o + (prow0 + row) * DH;
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) *reinterpret_cast<f32x4 *>(orow + 16 * dt + 4 * lg) = st.o[qt][dt];
-      if (lg == 0) {
-        const size_t mrow =
-            ((static_cast<size_t>(b) * p.hkv + kvh) * p.rows + row) * p.nsplit_ml + split;
-        p.ws_m[mrow] = st.m[qt];  // -inf when no position was visible: weight 0 in the merge
-        p.ws_l[mrow] = st.l[qt];
-      }
+      write_piece_row<DH>(prec, p.rows, row, lg, st.o[qt], st.m[qt], st.l[qt]);
     }
   }
 }

@@ -111,8 +111,7 @@ das_status make_plan(const das_cache *c, const das_batch *b, int hq, int w,
     plan->nsplit = 0;
     plan->nsplit_ml = 0;
     // a piece record: the rows' fp16 outputs, then 16 bytes per row
-    plan->piece_stride = static_cast<int>(
-        align_up(static_cast<size_t>(plan->rows) * (c->head_dim * 2 + 16)));
+    plan->piece_stride = static_cast<int>(piece_record_bytes(plan->rows, c->head_dim));
     const size_t pieces = static_cast<size_t>(plan->piece_cap);
     plan->ws_o_bytes = pieces * plan->piece_stride;
     plan->ws_ml_bytes = 0;
@@ -172,9 +171,17 @@ das_status make_plan(const das_cache *c, const das_batch *b, int hq, int w,
       return DAS_ERR_SHAPE;
   }
   if (units * 64 > kMaxItems) return DAS_ERR_SHAPE;  // the merge: (sequence, KV head) x 64
+  plan->nsplit_ml = (plan->nsplit + 3) & ~3;
+  if (plan->path == DAS_PATH_MFMA) {
+    // one piece record per (sequence, KV head, split)
+    plan->piece_stride = static_cast<int>(piece_record_bytes(plan->rows, c->head_dim));
+    plan->ws_o_bytes = static_cast<size_t>(units) * plan->nsplit * plan->piece_stride;
+    plan->ws_ml_bytes = 0;
+    plan->total = plan->ws_o_bytes;
+    return DAS_OK;
+  }
   const size_t per_split_rows =
       static_cast<size_t>(b->batch) * c->num_kv_heads * plan->nsplit * plan->rows;
-  plan->nsplit_ml = (plan->nsplit + 3) & ~3;
   plan->ws_o_bytes = align_up(per_split_rows * c->head_dim * sizeof(float));
   plan->ws_ml_bytes = align_up(static_cast<size_t>(b->batch) * c->num_kv_heads * plan->rows *
                                plan->nsplit_ml * sizeof(float));
@@ -259,7 +266,8 @@ das_status launch_attn(AttnParams p, const Plan &plan, int dtype, int dh, void *
                             : launch_attn_valu(p, dtype, dh, stream);
   if (e != hipSuccess) return DAS_ERR_HIP;
   // one split per sequence: the attention kernel wrote every output itself
-  if (plan.nsplit > 1 && launch_attn_combine(p, dtype, dh, 1, stream) != hipSuccess)
+  if (plan.nsplit > 1 && (mfma ? launch_attn_combine_records(p, dh, 1, stream)
+                              : launch_attn_combine(p, dtype, dh, 1, stream)) != hipSuccess)
     return DAS_ERR_HIP;
   return DAS_OK;
 }

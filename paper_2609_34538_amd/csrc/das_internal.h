@@ -27,7 +27,7 @@ struct AttnParams {
   const int32_t *block_table;  // [B][max_pages]
   uint32_t *dev_error;         // or nullptr
   float *ws_o;           // [B][Hkv][nsplit][rows][dh]     unnormalised partial O
-                         // (balanced schedule: piece records, see piece_stride)
+                         // (matrix-core kernels: piece records, see piece_stride)
   float *ws_m;           // [B][Hkv][rows][nsplit_ml]      running max (log2 units)
   float *ws_l;           // [B][Hkv][rows][nsplit_ml]      running sum
   int32_t batch, hq, hkv, group, w, rows;  // rows = w * group
@@ -36,10 +36,11 @@ struct AttnParams {
   int32_t nsplit_ml;     // nsplit rounded up to a multiple of 4 (16-byte rows of m, l)
   float scale_log2;      // log2(e) / sqrt(dh): logits in base-2 units
   // balanced schedule only: workers launched (one single-wave workgroup
-  // each), the piece capacity of the workspace and the bytes of one piece
-  // record at ws_o (the record: [rows][dh] fp16 scaled normalised output,
-  // then [rows] x {m, l, q, 0} fp32; records are 256-byte aligned)
-  int32_t n_workers, piece_cap, piece_stride;
+  // each) and the piece capacity of the workspace
+  int32_t n_workers, piece_cap;
+  // matrix-core kernels: bytes of one piece record at ws_o
+  // (piece_record_bytes; split grid: record (b * Hkv + kvh) * nsplit + split)
+  int32_t piece_stride;
   int32_t *ws_rec;       // balanced schedule: per unit {first piece, piece count}
 };
 
@@ -81,6 +82,9 @@ hipError_t launch_attn_mfma(const AttnParams &p, int dh, hipStream_t s);
 // by the attention kernel (both kernel families write them directly).
 hipError_t launch_attn_combine(const AttnParams &p, int dtype, int dh, int skip_single,
                                hipStream_t s);
+// The same over the piece records the matrix-core kernel writes (bf16 output).
+hipError_t launch_attn_combine_records(const AttnParams &p, int dh, int skip_single,
+                                       hipStream_t s);
 hipError_t launch_kv_append(const AppendParams &p, int dtype, int dh, hipStream_t s);
 // Balanced persistent schedule for batches of up to 64 sequences with blocks
 // of at most balanced_max_rows(dh) query rows (bf16): the attention kernel
@@ -89,6 +93,12 @@ hipError_t launch_attn_balanced(const AttnParams &p, int dh, hipStream_t s);
 constexpr int kBalancedMaxBatch = 64;
 // query rows per (sequence, KV head) the balanced kernel takes
 __host__ __device__ constexpr int balanced_max_rows(int dh) { return dh == 128 ? 16 : 32; }
+// Bytes of one piece record of the matrix-core kernels (a partial result
+// over part of a unit's positions): [rows][dh] fp16 outputs, then 16 bytes
+// per row, 256-byte aligned.
+__host__ __device__ constexpr size_t piece_record_bytes(int rows, int dh) {
+  return (static_cast<size_t>(rows) * (2 * dh + 16) + 255) / 256 * 256;
+}
 constexpr int kNumCUs = 256;  // compute units of an MI355X (gfx950)
 // Workers of the balanced schedule per compute unit: as many of its
 // single-wave workgroups as the 160 KB of LDS hold (two ring slots of

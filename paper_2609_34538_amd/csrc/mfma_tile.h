@@ -95,6 +95,41 @@ __device__ __forceinline__ float group_sum(float x) {
   return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
+typedef _Float16 h16x4 __attribute__((ext_vector_type(4)));
+
+// One query row of a piece record (piece_record_bytes): the row's normalised
+// output O / l in fp16, scaled by 2^-e so that its largest magnitude lies in
+// [2^14, 2^15) (full fp16 precision for the row whatever the value scale,
+// half the bytes of fp32 partials), and {m, l, q = l 2^e, 0}; the merge takes
+// the row's unnormalised output as the stored values times q. m = -inf and
+// l = 0 when no position was visible (weight 0 in the merge). Lane (n, g)
+// holds head dims 16 dt + 4 g .. + 3 of the row; the 4 lanes of a row call
+// this together (the row maximum is a 4-lane reduction).
+template <int DH>
+__device__ __forceinline__ void write_piece_row(uint8_t *rec, int rows, int row, int lg,
+                                                const f32x4 (&o)[DH / 16], float m, float l) {
+  const float inv = l > 0.f ? 1.f / l : 0.f;
+  float amax = 0.f;
+#pragma unroll
+  for (int dt = 0; dt < DH / 16; ++dt)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) amax = fmaxf(amax, fabsf(o[dt][v]));
+  amax = group_max(amax) * inv;
+  const int e = (amax > 0.f && amax <= 3.4e38f) ? __builtin_amdgcn_frexp_expf(amax) - 15 : 0;
+  const float sc = __builtin_amdgcn_ldexpf(inv, -e);
+  _Float16 *orow = reinterpret_cast<_Float16 *>(rec) + row * DH;
+#pragma unroll
+  for (int dt = 0; dt < DH / 16; ++dt) {
+    const h16x4 hv = {static_cast<_Float16>(o[dt][0] * sc), static_cast<_Float16>(o[dt][1] * sc),
+                      static_cast<_Float16>(o[dt][2] * sc), static_cast<_Float16>(o[dt][3] * sc)};
+    *reinterpret_cast<h16x4 *>(orow + 16 * dt + 4 * lg) = hv;
+  }
+  if (lg == 0) {
+    const f32x4 meta = {m, l, __builtin_amdgcn_ldexpf(l, e), 0.f};
+    *reinterpret_cast<f32x4 *>(rec + static_cast<size_t>(rows) * DH * 2 + row * 16) = meta;
+  }
+}
+
 template <int DH, int NQ, int NB_>
 struct Geo {
   static constexpr int KS = DH / 32;       // k steps of Q K^T

@@ -85,6 +85,10 @@ def test_workspace_size_formula():
     al = lambda x: (x + 255) // 256 * 256
     # partial O per split and row; m and l per row with the splits padded to 4
     assert ws_bytes(c, b, opts=o) == al(per * dh * 4) + 2 * al(B * hkv * rows * 12 * 4)
+    # the matrix-core kernel: a piece record per (sequence, KV head, split) of
+    # fp16 outputs and 16 bytes per row, 256-byte aligned
+    o.path = 2
+    assert ws_bytes(c, b, opts=o) == B * hkv * (maxp + 1) * al(rows * (dh * 2 + 16))
 
 
 def _nsplit_default(B, hkv, maxp, path=2, hq=None, w=8):
@@ -92,11 +96,16 @@ def _nsplit_default(B, hkv, maxp, path=2, hq=None, w=8):
     hq = hkv if hq is None else hq
     o = DasOptionsC()
     o.path, o.pages_per_split = path, 0
-    per_split = B * hkv * w * (hq // hkv)  # rows of one split
+    rows = w * (hq // hkv)
+    per_split = B * hkv * rows  # rows of one split
     n = ws_bytes(c, b, hq=hq, w=w, opts=o)
+    al = lambda x: (x + 255) // 256 * 256
     for ns in range(1, maxp + 2):
-        al = lambda x: (x + 255) // 256 * 256
-        if al(per_split * ns * 128 * 4) + 2 * al(per_split * ((ns + 3) // 4 * 4) * 4) == n:
+        if path == 2:  # one piece record per (sequence, KV head, split)
+            size = B * hkv * ns * al(rows * (128 * 2 + 16))
+        else:          # fp32 partials; m and l per row with the splits padded to 4
+            size = al(per_split * ns * 128 * 4) + 2 * al(per_split * ((ns + 3) // 4 * 4) * 4)
+        if size == n:
             return ns
     raise AssertionError("no split count matches the workspace size")
 

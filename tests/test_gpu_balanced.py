@@ -42,12 +42,14 @@ def test_long_sequence_among_short_ones(hkv, dh, w):
     assert_lse_close(lse, ref_lse, "long among short lse")
 
 
+@pytest.mark.parametrize("path,pps", [("balanced", 0), ("mfma", 4)])
 @pytest.mark.parametrize("v_scale", [2.0 ** -20, 2.0 ** 17, 3.0e5])
-def test_piece_scale_over_value_magnitudes(v_scale):
-    """Pieces keep O / l in fp16 under a per-row power-of-two scale: values
-    far below fp16's normal range and far above its largest finite value
-    merge as accurately as unit-scale ones (outputs compared after dividing
-    by the value scale; lse does not depend on it)."""
+def test_piece_scale_over_value_magnitudes(v_scale, path, pps):
+    """Pieces (balanced schedule) and split records (split grid) keep O / l
+    in fp16 under a per-row power-of-two scale: values far below fp16's
+    normal range and far above its largest finite value merge as accurately
+    as unit-scale ones (outputs compared after dividing by the value scale;
+    lse does not depend on it)."""
     lens = [40000, 64, 700]
     wl = dg.scaled(dg.WORKLOADS[3], batch=len(lens), hq=2, hkv=2, dh=96, layers=1,
                    prefix=(0, max(lens)), draft_depths=(2,), draft_widths=(16,),
@@ -59,10 +61,12 @@ def test_piece_scale_over_value_magnitudes(v_scale):
     q, kb, vb = dg.block_inputs(cd, 16, 2, DEV)
     vb = (vb.float() * v_scale).to(vb.dtype)
     lse = torch.empty((wl.batch, wl.hq, 16), dtype=torch.float32, device=DEV)
-    out = das.attn_policy(cache, batch, 0, 2, wl.depth_R, q, kb, vb, lse=lse, path="balanced")
+    out = das.attn_policy(cache, batch, 0, 2, wl.depth_R, q, kb, vb, lse=lse, path=path,
+                          pages_per_split=pps)
     torch.cuda.synchronize()
     ref, ref_lse = oracle_call(cd, 0, 2, wl.depth_R, q, kb, vb, range(wl.batch))
-    assert_close(out.double() / v_scale, ref / v_scale, wl.dtype, f"value scale {v_scale:g}")
+    assert_close(out.double() / v_scale, ref / v_scale, wl.dtype,
+                 f"{path} value scale {v_scale:g}")
     assert_lse_close(lse, ref_lse, f"value scale {v_scale:g} lse")
 
 

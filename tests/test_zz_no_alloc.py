@@ -53,13 +53,13 @@ def test_noalloc_matches_policy_on_two_calls(dtype, path):
 
 
 def test_noalloc_rejects_requests_beyond_the_scratch():
-    # 32 sequences x 55 KV heads x 32 rows x 5 splits of fp32 partials: > 64 MiB
+    # 32 sequences x 55 KV heads x 9 splits of 32-row piece records: > 64 MiB
     hkv, dh, w = 55, 96, 32
     k_pool = torch.zeros((1, 1, hkv, 1, 64, dh), dtype=torch.bfloat16, device=DEV)
     v_pool = torch.zeros((1, 1, hkv, 1, 8, dh, 8), dtype=torch.bfloat16, device=DEV)
     cache = das.PagedCache(k_pool, v_pool, 32, {32: 0}, {32: 0})
     batch = das.Batch(torch.zeros(32, dtype=torch.int32, device=DEV),
-                      torch.zeros((32, 129), dtype=torch.int32, device=DEV))
+                      torch.zeros((32, 257), dtype=torch.int32, device=DEV))
     # on the split grid (the balanced schedule's pieces fit)
     assert das.workspace_bytes(cache, batch, hkv, w, path="mfma") > das.NOALLOC_SCRATCH_BYTES
     assert das.workspace_bytes(cache, batch, hkv, w) <= das.NOALLOC_SCRATCH_BYTES
