@@ -54,10 +54,10 @@ TRAFFIC_SOURCES = ["paper_2609_34538_amd/csrc/attn_mfma.hip",
                    "paper_2609_34538_amd/csrc/mfma_tile.h",
                    "paper_2609_34538_amd/csrc/das_api.hip",
                    "paper_2609_34538_amd/csrc/das_internal.h"]
-MEASURED_TRAFFIC = {("das-wave-step-bf16", "93951a37267e7167"): 4_512_325_279,
-                    ("long-prefix-gqa-bf16", "93951a37267e7167"): 344_385_565,
-                    ("ragged-paged-bf16", "93951a37267e7167"): 859_773_684,
-                    ("single-seq-looped-bf16", "93951a37267e7167"): 47_885_685}
+MEASURED_TRAFFIC = {("das-wave-step-bf16", "f55ce52654c4a5e9"): 4_486_439_990,
+                    ("long-prefix-gqa-bf16", "f55ce52654c4a5e9"): 309_900_217,
+                    ("ragged-paged-bf16", "f55ce52654c4a5e9"): 839_975_327,
+                    ("single-seq-looped-bf16", "f55ce52654c4a5e9"): 47_026_088}
 
 
 def kernel_digest():
