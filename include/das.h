@@ -174,9 +174,11 @@ typedef struct das_attn_options {
 } das_attn_options;
 
 /*
- * Bytes of device workspace an attention call with these shapes needs
- * (fp32 partial results of the prefix splits). Returns 0 for arguments that
- * the attention entry points would reject. `opts` may be NULL.
+ * Bytes of device workspace an attention call with these shapes needs (the
+ * partial results of the prefix splits or pieces: fp16 records with fp32
+ * maxima and sums on the matrix-core paths, fp32 on the vector-ALU path).
+ * Returns 0 for arguments that the attention entry points would reject.
+ * `opts` may be NULL.
  */
 size_t das_attn_workspace_bytes(const das_cache *cache, const das_batch *batch,
                                 int32_t num_q_heads, int32_t block_len);

@@ -75,7 +75,7 @@ struct Plan {
   int nsplit_ml;        // nsplit rounded up to a multiple of 4
   int n_workers;        // balanced schedule: workers launched
   int piece_cap;        // balanced schedule: pieces the workspace holds
-  int piece_stride;     // balanced schedule: bytes of one piece record
+  int piece_stride;     // matrix-core kernels: bytes of one piece record
   size_t ws_o_bytes, ws_ml_bytes, ws_rec_bytes, total;
 };
 
