@@ -6,8 +6,9 @@
 // unit has 2 * ceil(S_b / 64) prefix tiles of 32 tokens (two per page) and
 // ceil(w / 32) block tiles, in that order. The units of all sequences, laid
 // end to end (sequence-major, then KV head), form one global sequence of T
-// tiles. Worker j of W (one single-wave workgroup per resident wave slot of
-// the chip) takes the tiles [T j / W, T (j + 1) / W): every worker streams
+// tiles. Worker j of W (single-wave workgroups, balanced_workers_per_cu of
+// them per compute unit, all resident at once) takes the tiles
+// [T j / W, T (j + 1) / W): every worker streams
 // the same number of tiles (+-1), whatever the lengths, so the launch has no
 // tail of long chunks and no idle slots while short ones finish.
 //
@@ -15,10 +16,9 @@
 // loads of the chunked kernel) without pausing at unit boundaries: while
 // tile k is computed, tile k + 1 is loaded into the other slot, and so are
 // the page id of tile k + 2 and, when tile k + 1 opens a new unit, that
-// unit's Q rows. One tile in flight per wave, all six waves of a compute
-// unit busy: on the batched workloads this measured faster than keeping two
-// tiles in flight (the chunked kernel's depth), 0.72-0.73 against 0.68-0.69
-// of 8 TB/s on the same box. At the end
+// unit's Q rows. One tile in flight per wave: on the batched workloads this
+// measured faster than keeping two tiles in flight (the chunked kernel's
+// depth), 0.72-0.73 against 0.68-0.69 of 8 TB/s on the same box. At the end
 // of a unit (or of its range) the worker writes the unit's normalised output
 // when it processed the whole unit, otherwise a piece (the running maximum
 // m, the sum l and the normalised output O / l in fp16 under a per-row

@@ -275,8 +275,8 @@ def test_attention_grid_limits():
 
 
 def test_balanced_schedule_workspace_and_limits():
-    # pieces = sequences x KV heads + workers (256 CUs x the single-wave
-    # workgroups whose two ring slots fit in 160 KB: 6 at head dim 96, 5 at 128)
+    # pieces = sequences x KV heads + workers (256 CUs x 512 / head_dim
+    # single-wave workgroups: 5 at head dim 96, 4 at 128)
     o = DasOptionsC()
     o.path, o.pages_per_split = 3, 0
     al = lambda x: (x + 255) // 256 * 256
@@ -284,14 +284,14 @@ def test_balanced_schedule_workspace_and_limits():
     rows = 16 * 2  # w 16, G 2
     # a piece record per piece (fp16 outputs + 16 bytes per row, 256-byte
     # aligned), plus a {first piece, piece count} record per (sequence, KV head)
-    pieces = 4 * 8 + 256 * 6
+    pieces = 4 * 8 + 256 * 5
     rec = al(4 * 8 * 8)
     assert ws_bytes(c, b, hq=16, w=16, opts=o) == pieces * al(rows * (96 * 2 + 16)) + rec
     c128 = make_cache(hkv=8, dh=128)
-    pieces = 4 * 8 + 256 * 5
+    pieces = 4 * 8 + 256 * 4
     assert ws_bytes(c128, b, hq=8, w=16, opts=o) == pieces * al(16 * (128 * 2 + 16)) + rec
     # odd row counts: records stay 256-byte aligned
-    assert ws_bytes(c, b, hq=8, w=3, opts=o) == (4 * 8 + 256 * 6) * al(3 * (96 * 2 + 16)) + rec
+    assert ws_bytes(c, b, hq=8, w=3, opts=o) == (4 * 8 + 256 * 5) * al(3 * (96 * 2 + 16)) + rec
     # limits: 64 sequences, 32 query rows (16 at head dim 128)
     assert ws_bytes(c, make_batch(B=64, maxp=10), hq=8, w=32, opts=o) > 0
     assert ws_bytes(c, make_batch(B=65, maxp=10), hq=8, w=32, opts=o) == 0
