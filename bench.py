@@ -54,10 +54,10 @@ TRAFFIC_SOURCES = ["paper_2609_34538_amd/csrc/attn_mfma.hip",
                    "paper_2609_34538_amd/csrc/mfma_tile.h",
                    "paper_2609_34538_amd/csrc/das_api.hip",
                    "paper_2609_34538_amd/csrc/das_internal.h"]
-MEASURED_TRAFFIC = {("das-wave-step-bf16", "80c4eccbac8d5bc2"): 4_486_439_990,
-                    ("long-prefix-gqa-bf16", "80c4eccbac8d5bc2"): 309_900_217,
-                    ("ragged-paged-bf16", "80c4eccbac8d5bc2"): 839_975_327,
-                    ("single-seq-looped-bf16", "80c4eccbac8d5bc2"): 47_026_088}
+MEASURED_TRAFFIC = {("das-wave-step-bf16", "7009de5c6cf03d84"): 4_471_134_404,
+                    ("long-prefix-gqa-bf16", "7009de5c6cf03d84"): 309_934_659,
+                    ("ragged-paged-bf16", "7009de5c6cf03d84"): 834_919_618,
+                    ("single-seq-looped-bf16", "7009de5c6cf03d84"): 47_023_131}
 
 
 def kernel_digest():
