@@ -115,7 +115,7 @@ __device__ __forceinline__ void write_piece_row(uint8_t *rec, int rows, int row,
 #pragma unroll
     for (int v = 0; v < 4; ++v) amax = fmaxf(amax, fabsf(o[dt][v]));
   amax = group_max(amax) * inv;
-  const int e = (amax > 0.f && amax <= 3.4e38f) ? __builtin_amdgcn_frexp_expf(amax) - 15 : 0;
+  const int e = (amax > 0.f && amax < __builtin_huge_valf()) ? __builtin_amdgcn_frexp_expf(amax) - 15 : 0;
   const float sc = __builtin_amdgcn_ldexpf(inv, -e);
   _Float16 *orow = reinterpret_cast<_Float16 *>(rec) + row * DH;
 #pragma unroll

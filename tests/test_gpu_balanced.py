@@ -43,7 +43,7 @@ def test_long_sequence_among_short_ones(hkv, dh, w):
 
 
 @pytest.mark.parametrize("path,pps", [("balanced", 0), ("mfma", 4)])
-@pytest.mark.parametrize("v_scale", [2.0 ** -20, 2.0 ** 17, 3.0e5])
+@pytest.mark.parametrize("v_scale", [2.0 ** -100, 2.0 ** -20, 2.0 ** 17, 3.0e5, 2.0 ** 100])
 def test_piece_scale_over_value_magnitudes(v_scale, path, pps):
     """Pieces (balanced schedule) and split records (split grid) keep O / l
     in fp16 under a per-row power-of-two scale: values far below fp16's
