@@ -1,7 +1,7 @@
 """Calls captured into a HIP graph and replayed give the same bytes as the
-same calls launched eagerly: draft and verifier attention (split prefix, so
-the combine kernel runs too) and the commit. Every replay is checked, with
-eager work and synchronisations between replays."""
+same calls launched eagerly: draft and verifier attention (split prefix or
+balanced schedule, so a merge kernel runs too) and the commit. Every replay
+is checked, with eager work and synchronisations between replays."""
 
 from __future__ import annotations
 
@@ -16,8 +16,9 @@ pytestmark = pytest.mark.gpu
 DEV = "cuda"
 
 
-@pytest.mark.parametrize("path", ["valu", "mfma"])
+@pytest.mark.parametrize("path", ["valu", "mfma", "balanced"])
 def test_graph_replay_matches_eager(path):
+    pps = 0 if path == "balanced" else 2
     wl = dg.scaled(dg.WORKLOADS[5], batch=5, hq=6, hkv=3, layers=2, prefix=(0, 400))
     torch.manual_seed(0)
     cd = dg.make_cache(wl, DEV, prefix_lens=[0, 65, 200, 333, 400])
@@ -28,7 +29,7 @@ def test_graph_replay_matches_eager(path):
     k_new, v_new, num_new = dg.commit_inputs(cd, 16, DEV)
     num_new_t = torch.as_tensor(num_new, device=DEV)
     kp, vp = cd.k_plane[R], cd.v_plane[R]
-    ws = das.alloc_workspace(cache, batch, wl.hq, 16, path=path, pages_per_split=2)
+    ws = das.alloc_workspace(cache, batch, wl.hq, 16, path=path, pages_per_split=pps)
     out_d = torch.empty_like(qd)
     out_v = torch.empty_like(qv)
     lse_d = torch.empty((wl.batch, wl.hq, 8), dtype=torch.float32, device=DEV)
@@ -37,9 +38,9 @@ def test_graph_replay_matches_eager(path):
     torch.cuda.synchronize()
     calls = [
         das.PreparedAttention(cache, batch, 1, 2, R, qd, kbd, vbd, out_d, ws, lse=lse_d,
-                              path=path, pages_per_split=2, stream=stream),
+                              path=path, pages_per_split=pps, stream=stream),
         das.PreparedAttention(cache, batch, 0, R, R, qv, k_new[kp, 0], v_new[vp, 0], out_v, ws,
-                              path=path, pages_per_split=2, stream=stream),
+                              path=path, pages_per_split=pps, stream=stream),
         das.PreparedAppend(cache, batch, k_new, v_new, num_new_t, len_out, stream=stream),
     ]
     k0, v0 = cd.k_pool.clone(), cd.v_pool.clone()
