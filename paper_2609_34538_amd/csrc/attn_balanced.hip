@@ -13,12 +13,14 @@
 // tail of long chunks and no idle slots while short ones finish.
 //
 // A worker streams its tiles through a two-slot LDS ring (the direct-to-LDS
-// loads of the chunked kernel) without pausing at unit boundaries: while
-// tile k is computed, tile k + 1 is loaded into the other slot, and so are
-// the page id of tile k + 2 and, when tile k + 1 opens a new unit, that
-// unit's Q rows. One tile in flight per wave: on the batched workloads this
-// measured faster than keeping two tiles in flight (the chunked kernel's
-// depth), 0.72-0.73 against 0.68-0.69 of 8 TB/s on the same box. At the end
+// loads of the split-grid kernel) without pausing at unit boundaries: while
+// tile k is computed, tile k + 1 is loaded into the other slot. Page ids come
+// from a 64-entry window in registers; the unit's next window, the next
+// unit's first window and (one row tile per wave) the next unit's Q rows are
+// loaded a window or a unit ahead. One tile in flight per wave: on the
+// batched workloads this measured faster than keeping two tiles in flight
+// (the split-grid kernel's depth), 0.72-0.73 against 0.68-0.69 of 8 TB/s on
+// the same box. At the end
 // of a unit (or of its range) the worker writes the unit's normalised output
 // when it processed the whole unit, otherwise a piece (the running maximum
 // m, the sum l and the normalised output O / l in fp16 under a per-row
@@ -153,31 +155,15 @@ void attn_balanced_kernel(AttnParams p) {
     c0.kvh = static_cast<int>(local / c0.tu);
     c0.t = static_cast<int>(local % c0.tu);
   }
-  auto advance = [&](Cursor &x) {
-    if (++x.t < x.tu) return;
-    x.t = 0;
-    if (++x.kvh < p.hkv) return;
-    x.kvh = 0;
-    if (++x.b >= p.batch) return;  // past the last tile: never used
-    x.s = __builtin_amdgcn_readlane(tm.s, x.b);
-    x.np = (x.s + kPage - 1) / kPage;
-    x.tu = __builtin_amdgcn_readlane(tm.tu, x.b);
-  };
-
   const char *kl = static_cast<const char *>(p.k_layer);
   const char *vl = static_cast<const char *>(p.v_layer);
   const size_t tok_bytes = static_cast<size_t>(p.hkv) * DH * 2;  // block row stride
   // per-lane byte offsets of a fragment inside a page half (as in the
-  // chunked kernel): key token slot 8(n/4) + n%4, column 8g; value token
+  // split-grid kernel): key token slot 8(n/4) + n%4, column 8g; value token
   // group g, head dim n
   const uint32_t lane_k = ((8 * (ln >> 2) + (ln & 3)) * DH + 8 * lg) * 2;
   const uint32_t lane_v = (lg * DH + ln) * 16;
 
-  // page id of a prefix tile (0 for block tiles); read by every lane
-  auto load_pid = [&](const Cursor &x) -> int {
-    if (x.t >= 2 * x.np) return 0;
-    return p.block_table[static_cast<size_t>(x.b) * p.max_pages + (x.t >> 1)];
-  };
   // Q fragments of a unit (B operand of S^T = K Q^T: lane holds dims
   // 8g..8g+7 of row n); rows past the block's last are clamped and never
   // written
@@ -489,7 +475,7 @@ void attn_balanced_kernel(AttnParams p) {
   }
 }
 
-// Merge of a unit's pieces (as the chunked kernel's merge, over the pieces
+// Merge of a unit's pieces (as the split-grid kernel's merge, over the pieces
 // of the workers that share the unit): one 256-thread workgroup per unit,
 // each thread holding IT (row, 4 columns) items and issuing the loads of all
 // of them at once, so the merge costs two memory round trips (the record,
