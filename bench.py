@@ -78,8 +78,9 @@ def kernel_digest():
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=None,
+                    help="timed steps (default: 20 for workload 5, 50 for the others)")
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--config", type=int, default=5, help="workload index (1-5)")
     ap.add_argument("--path", default="auto", choices=["auto", "valu", "mfma"])
     ap.add_argument("--pps", type=int, default=0, help="prefix pages per split (0 = library)")
@@ -104,7 +105,10 @@ def parse():
                     help="greedy acceptance on the device; its commit counts feed the commit")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only copy 1 GiB device to device once (reference for HBM counters)")
-    return ap.parse_args()
+    args = ap.parse_args()
+    if args.steps is None:
+        args.steps = 20 if args.config == 5 else 50
+    return args
 
 
 def algorithmic_attn_bytes(wl, lens, w):
