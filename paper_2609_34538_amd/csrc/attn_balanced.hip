@@ -25,7 +25,11 @@
 // when it processed the whole unit, otherwise a piece (the running maximum
 // m, the sum l and the normalised output O / l in fp16 under a per-row
 // power-of-two scale) that the merge kernel combines with the unit's other
-// pieces.
+// pieces. Only the range's first unit can end as a piece in the middle of
+// the range; its record waits in LDS and is written with the range's last
+// flush, because writes in the middle of the stream delay the reads at the
+// DRAM (width-32 calls 0.768 -> 0.788 and 0.771 -> 0.805 of 8 TB/s, ragged
+// batch 0.702 -> 0.720, same process).
 // Pieces are indexed unit + worker: along the tile sequence either the unit
 // or the worker (or both) advances, so the index is unique, and a unit's
 // pieces are consecutive.
@@ -129,6 +133,13 @@ void attn_balanced_kernel(AttnParams p) {
   constexpr int KS = G::KS;
   constexpr int DT = G::DT;
   __shared__ __attribute__((aligned(16))) uint8_t ring[2 * G::SLOT];
+  // the record of a piece that ends in the middle of the range (only the
+  // range's first unit can), written to global memory with the range's last
+  // flush
+  constexpr int kStash = static_cast<int>(piece_record_bytes(balanced_max_rows(DH), DH));
+  __shared__ __attribute__((aligned(16))) uint8_t stash[kStash];
+  static_assert(2 * G::SLOT + kStash == balanced_lds_per_worker(DH),
+                "the host's worker count assumes this LDS per worker");
 
   const int lane = threadIdx.x;
   const int ln = lane & 15;
@@ -256,8 +267,7 @@ void attn_balanced_kernel(AttnParams p) {
   // End of a unit's stretch in this worker: the normalised output when the
   // worker processed the whole unit, else a piece for the merge. Lane holds
   // head dims 16dt + 4g .. +3 of row n of tile qt.
-  auto flush = [&](const Cursor &x, bool whole) {
-    const size_t piece = static_cast<size_t>(x.b) * p.hkv + x.kvh + j;
+  auto flush = [&](const Cursor &x, bool whole, uint8_t *rec) {
 #pragma unroll
     for (int qt = 0; qt < NQ; ++qt) {
       const int row = qt * 16 + ln;
@@ -285,8 +295,7 @@ void attn_balanced_kernel(AttnParams p) {
         // written by this wave alone), in half the bytes of fp32 partials:
         // the stores of a piece written in the middle of a worker's range
         // delay its next tile waits
-        write_piece_row<DH>(reinterpret_cast<uint8_t *>(p.ws_o) + piece * p.piece_stride, p.rows,
-                            row, lg, st.o[qt], st.m[qt], st.l[qt]);
+        write_piece_row<DH>(rec, p.rows, row, lg, st.o[qt], st.m[qt], st.l[qt]);
       }
     }
   };
@@ -345,6 +354,7 @@ void attn_balanced_kernel(AttnParams p) {
     for (int part = 0; part < 3; ++part) issue_part(0, cu, part, kbase, vbase);
   }
   long long g_unit = g0 - c0.t;  // global index of the current unit's first tile
+  uint8_t *stash_dst = nullptr;  // global record of the stashed piece
   int si = 0;                // ring slot of the tile being computed
   long long remaining = n;   // tiles left in this worker's range
   for (;;) {
@@ -450,7 +460,18 @@ void attn_balanced_kernel(AttnParams p) {
       });
       si = sn;
     }
-    flush(cu, t_first == 0 && t_end == cu.tu);
+    {
+      const bool whole = t_first == 0 && t_end == cu.tu;
+      const bool last = remaining <= t_end - t_first;
+      const size_t piece = static_cast<size_t>(cu.b) * p.hkv + cu.kvh + j;
+      uint8_t *grec = reinterpret_cast<uint8_t *>(p.ws_o) + piece * p.piece_stride;
+      if (!whole && !last && stash_dst == nullptr) {
+        flush(cu, false, stash);
+        stash_dst = grec;
+      } else {
+        flush(cu, whole, grec);
+      }
+    }
     if (t_first == 0 && lane == 0) {
       // this worker holds the unit's first tile: record where the unit's
       // pieces start and how many workers share it, for the merge
@@ -461,7 +482,14 @@ void attn_balanced_kernel(AttnParams p) {
     }
     g_unit += cu.tu;
     remaining -= t_end - t_first;
-    if (remaining <= 0) break;
+    if (remaining <= 0) {
+      if (stash_dst) {
+        const int bytes = p.rows * (DH * 2 + 16);
+        for (int off = 16 * lane; off < bytes; off += 1024)
+          *reinterpret_cast<u32x4 *>(stash_dst + off) = *reinterpret_cast<const u32x4 *>(stash + off);
+      }
+      break;
+    }
     cu = nu;
     pwin = pwin_n;
     pw0 = 0;

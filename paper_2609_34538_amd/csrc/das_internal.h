@@ -101,17 +101,24 @@ __host__ __device__ constexpr size_t piece_record_bytes(int rows, int dh) {
 }
 constexpr int kNumCUs = 256;  // compute units of an MI355X (gfx950)
 // Workers of the balanced schedule per compute unit: 64 KB of tiles in flight
-// per CU, one 128 * dh-byte tile per worker (8 at head dim 64, 5 at 96, 4 at
-// 128). Measured against the workers whose two ring slots fill the 160 KB of
-// LDS (10, 6, 5): 0.80 against 0.65, 0.80 against 0.80 and 0.80 against 0.61
-// of 8 TB/s on the DAS-Wave step's shape at each head dim; when the rings fill
-// the LDS exactly (head dims 64 and 128) a CU's last worker is not resident
-// with the others and runs after them.
-__host__ __device__ constexpr int balanced_workers_per_cu(int dh) { return 512 / dh; }
-static_assert(balanced_workers_per_cu(64) * 2 * 128 * 64 < 160 * 1024 &&
-                  balanced_workers_per_cu(96) * 2 * 128 * 96 < 160 * 1024 &&
-                  balanced_workers_per_cu(128) * 2 * 128 * 128 < 160 * 1024,
-              "the rings of a CU's workers fit its LDS");
+// per CU, one 128 * dh-byte tile per worker, as long as every worker's LDS
+// (two ring slots and one stashed piece record) fits strictly inside the
+// 160 KB: 7 at head dim 64, 5 at 96, 4 at 128. Measured against the workers
+// whose rings alone fill the LDS (10, 6, 5): 0.78 against 0.63, 0.78 against
+// 0.78 and 0.80 against 0.60 of 8 TB/s on the DAS-Wave step's shape at each
+// head dim; when the LDS is filled exactly (head dims 64 and 128) a CU's
+// last worker is not resident with the others and runs after them.
+__host__ __device__ constexpr int balanced_lds_per_worker(int dh) {
+  return 2 * 128 * dh + static_cast<int>(piece_record_bytes(balanced_max_rows(dh), dh));
+}
+__host__ __device__ constexpr int balanced_workers_per_cu(int dh) {
+  return 512 / dh < (160 * 1024 - 1) / balanced_lds_per_worker(dh)
+             ? 512 / dh
+             : (160 * 1024 - 1) / balanced_lds_per_worker(dh);
+}
+static_assert(balanced_workers_per_cu(64) == 7 && balanced_workers_per_cu(96) == 5 &&
+                  balanced_workers_per_cu(128) == 4,
+              "workers per CU of the balanced schedule");
 
 struct AcceptParams {
   const int32_t *proposals;    // [B][w]
