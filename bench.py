@@ -54,10 +54,10 @@ TRAFFIC_SOURCES = ["paper_2609_34538_amd/csrc/attn_mfma.hip",
                    "paper_2609_34538_amd/csrc/mfma_tile.h",
                    "paper_2609_34538_amd/csrc/das_api.hip",
                    "paper_2609_34538_amd/csrc/das_internal.h"]
-MEASURED_TRAFFIC = {("das-wave-step-bf16", "7bff112eb8735e22"): 4_470_974_034,
-                    ("long-prefix-gqa-bf16", "7bff112eb8735e22"): 309_883_924,
-                    ("ragged-paged-bf16", "7bff112eb8735e22"): 834_916_756,
-                    ("single-seq-looped-bf16", "7bff112eb8735e22"): 47_023_303}
+MEASURED_TRAFFIC = {("das-wave-step-bf16", "f411110f35c4b1a5"): 4_467_779_523,
+                    ("long-prefix-gqa-bf16", "f411110f35c4b1a5"): 309_886_458,
+                    ("ragged-paged-bf16", "f411110f35c4b1a5"): 834_081_758,
+                    ("single-seq-looped-bf16", "f411110f35c4b1a5"): 47_023_665}
 
 
 def kernel_digest():
