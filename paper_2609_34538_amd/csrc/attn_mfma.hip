@@ -68,8 +68,8 @@ __device__ __forceinline__ void prio_by_remaining(int rem) {
 // output and score accumulators stay in VGPRs (the MFMAs write them there)
 // instead of being copied out of AGPRs on every tile.
 // NW = 1: one wave per chunk, its own ring. NW > 1: the NW row tiles of a
-// split share one workgroup and one ring; each wave loads every NW-th
-// fragment of a tile and one barrier per tile both publishes the tile and
+// split share one workgroup and one ring; each wave loads its own block of
+// NF / NW consecutive fragments of a tile (whole 128-byte lines of the page) and one barrier per tile both publishes the tile and
 // frees the slot read in the previous iteration, which is then refilled
 // (NB - 1 tiles in flight).
 template <int DH, int NQ, int NB, int NW>
@@ -83,7 +83,7 @@ void attn_mfma_kernel(AttnParams p, int n_rg, int n_chunks) {
   __shared__ __attribute__((aligned(16))) uint8_t ring[NB * G::SLOT];
 
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform: scalar branches
   const int ln = lane & 15;
   const int lg = lane >> 4;
   const int pps = p.pages_per_split;
@@ -175,8 +175,11 @@ void attn_mfma_kernel(AttnParams p, int n_rg, int n_chunks) {
     kbase = kl + off + (32 * u) * DH * 2;
     vbase = vl + off + 64 * DH * u;
   };
-  // fragment f of a tile is loaded by wave f % NW
-  auto mine = [&](int f) { return NW == 1 || f % NW == wave; };
+  // fragment f of a tile is loaded by wave f / (NF / NW): a wave's fragments
+  // cover whole 128-byte lines (the key fragments of one S^T half are the
+  // 64-byte pieces of the same token rows), so no line is requested by two
+  // waves
+  auto mine = [&](int f) { return NW == 1 || f / (NF / NW) == wave; };
   // Loads of tile t into ring slot t % NB, in three parts (key fragments of
   // each S^T half, then the values) so they can be spread over the
   // computation of the previous tile. Both halves span 64 * DH bytes.
@@ -364,7 +367,7 @@ void attn_mfma_kernel(AttnParams p, int n_rg, int n_chunks) {
     }
     // the slot's fragments are in registers before the next barrier
     __builtin_amdgcn_s_waitcnt(0xF | (0x3 << 14) | (0x7 << 4));  // lgkmcnt(0)
-    compute_tile<DH, NQ>(st, kf, vf, qf, cap, limit, full, p.scale_log2, lg, [](int) {});
+    compute_tile<DH, NQ, true>(st, kf, vf, qf, cap, limit, full, p.scale_log2, lg, [](int) {});
   }
 
   }
