@@ -159,7 +159,10 @@ typedef enum das_attn_path {
                             blocks of at most 32 query rows, i.e.
                             w * Hq / Hkv <= 32, or 16 at head_dim 128;
                             DAS_ERR_UNSUPPORTED otherwise). DAS_PATH_AUTO takes it for batches
-                            of 2..64 sequences when pages_per_split is 0. */
+                            of 2..64 sequences when pages_per_split is 0
+                            and the batch has more than W / 8 (sequence,
+                            KV head) units, W = 256 x (7, 5, 4) workers
+                            at head_dim (64, 96, 128). */
 } das_attn_path;
 
 typedef struct das_attn_options {

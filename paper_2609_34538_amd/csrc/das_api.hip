@@ -53,16 +53,24 @@ das_status check_batch(const das_batch *b) {
 }
 
 // Which kernel family (and schedule) runs a request. The balanced schedule
-// serves ragged batches: every resident wave streams an equal share of all
-// tiles, so unequal prefix lengths leave no idle slots; a single sequence
-// has nothing to balance and keeps the split grid (one fewer dependent
-// memory round trip before its first tile).
+// serves batches with many (sequence, KV head) units: every resident wave
+// streams an equal share of all tiles, so unequal prefix lengths leave no
+// idle slots. With few units for the chip's workers (at most 8 workers per
+// unit) each worker holds a short run behind its dependent start-up round
+// trips and leaves one piece per unit it shares, and the split grid's
+// chunks, dealt out by the hardware dispatcher, are faster; a single
+// sequence has nothing to balance and keeps the split grid too.
+bool balanced_pays(const das_cache *c, const das_batch *b) {
+  return 8LL * b->batch * c->num_kv_heads >
+         static_cast<long long>(kNumCUs) * balanced_workers_per_cu(c->head_dim);
+}
+
 int choose_path(const das_cache *c, const das_batch *b, int rows, const das_attn_options *o) {
   const int want = o ? o->path : DAS_PATH_AUTO;
   if (c->dtype == DAS_F32) return DAS_PATH_VALU;
   if (want != DAS_PATH_AUTO) return want;
   if (b->batch >= 2 && b->batch <= kBalancedMaxBatch && rows <= balanced_max_rows(c->head_dim) &&
-      !(o && o->pages_per_split != 0))
+      !(o && o->pages_per_split != 0) && balanced_pays(c, b))
     return DAS_PATH_BALANCED;
   return DAS_PATH_MFMA;
 }

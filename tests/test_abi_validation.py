@@ -297,14 +297,19 @@ def test_balanced_schedule_workspace_and_limits():
     assert ws_bytes(c, make_batch(B=65, maxp=10), hq=8, w=32, opts=o) == 0
     assert ws_bytes(c, b, hq=8, w=33, opts=o) == 0
     assert ws_bytes(c128, b, hq=8, w=17, opts=o) == 0
-    # library choice: the balanced schedule for 2..64 sequences, the split
-    # grid otherwise (its workspace is sized per split)
+    # library choice: the balanced schedule for 2..64 sequences with more
+    # than W / 8 (sequence, KV head) units (W = 1280 workers at head dim 96,
+    # 1024 at 128), the split grid otherwise (its workspace is sized per split)
     o.path = 0
-    assert ws_bytes(c, b, hq=16, w=16, opts=o) == ws_bytes(c, b, hq=16, w=16, opts=_opts(3))
-    assert ws_bytes(c, make_batch(B=1), hq=16, w=16, opts=o) == \
-        ws_bytes(c, make_batch(B=1), hq=16, w=16, opts=_opts(2))
+    for B, path in ((21, 3), (20, 2), (4, 2), (1, 2)):
+        bb = make_batch(B=B, maxp=10)
+        assert ws_bytes(c, bb, hq=16, w=16, opts=o) == ws_bytes(c, bb, hq=16, w=16, opts=_opts(path)), B
+    for B, path in ((17, 3), (16, 2)):
+        bb = make_batch(B=B, maxp=10)
+        assert ws_bytes(c128, bb, hq=8, w=16, opts=o) == ws_bytes(c128, bb, hq=8, w=16, opts=_opts(path)), B
     o.pages_per_split = 4
-    assert ws_bytes(c, b, hq=16, w=16, opts=o) == ws_bytes(c, b, hq=16, w=16, opts=_opts(2, 4))
+    big = make_batch(B=21, maxp=10)
+    assert ws_bytes(c, big, hq=16, w=16, opts=o) == ws_bytes(c, big, hq=16, w=16, opts=_opts(2, 4))
     # fp32 caches have no balanced schedule
     assert ws_bytes(make_cache(dtype=0), b, opts=_opts(3)) == 0
 

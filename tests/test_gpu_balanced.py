@@ -90,10 +90,12 @@ def test_all_prefixes_empty():
 
 def test_library_choice_and_determinism():
     """The library takes the balanced schedule for a batch of 2..64 sequences
-    (bit-identical to asking for it) and the split grid when a split size is
-    given; repeated calls agree bit for bit."""
+    with more than W / 8 (sequence, KV head) units (bit-identical to asking
+    for it), the split grid for fewer units or when a split size is given;
+    repeated calls agree bit for bit."""
     lens = [1500, 333, 4096, 0, 2047]
-    wl, cd, (cache, batch, q, kb, vb), out, _ = _run(lens, 4, 4, 96, 16)
+    # 5 x 40 = 200 units > 1280 / 8 at head dim 96
+    wl, cd, (cache, batch, q, kb, vb), out, _ = _run(lens, 40, 40, 96, 16)
     auto = das.attn_policy(cache, batch, 0, 2, wl.depth_R, q, kb, vb)
     again = das.attn_policy(cache, batch, 0, 2, wl.depth_R, q, kb, vb, path="balanced")
     grid = das.attn_policy(cache, batch, 0, 2, wl.depth_R, q, kb, vb, pages_per_split=4)
@@ -103,6 +105,15 @@ def test_library_choice_and_determinism():
     assert torch.equal(auto.view(torch.int16), out.view(torch.int16))
     assert torch.equal(again.view(torch.int16), out.view(torch.int16))
     assert torch.equal(grid.view(torch.int16), grid_ref.view(torch.int16))
+    # 5 x 4 = 20 units: the split grid with the library's split size
+    wl, cd, (cache, batch, q, kb, vb), bal, _ = _run(lens, 4, 4, 96, 16)
+    auto = das.attn_policy(cache, batch, 0, 2, wl.depth_R, q, kb, vb)
+    grid = das.attn_policy(cache, batch, 0, 2, wl.depth_R, q, kb, vb, path="mfma")
+    torch.cuda.synchronize()
+    assert torch.equal(auto.view(torch.int16), grid.view(torch.int16))
+    ref, _ = oracle_call(cd, 0, 2, wl.depth_R, q, kb, vb, range(wl.batch))
+    assert_close(auto, ref, wl.dtype, "library choice, few units")
+    assert_close(bal, ref, wl.dtype, "balanced, few units")
 
 
 def test_unsupported_shapes_are_refused():
