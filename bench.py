@@ -54,10 +54,10 @@ TRAFFIC_SOURCES = ["paper_2609_34538_amd/csrc/attn_mfma.hip",
                    "paper_2609_34538_amd/csrc/mfma_tile.h",
                    "paper_2609_34538_amd/csrc/das_api.hip",
                    "paper_2609_34538_amd/csrc/das_internal.h"]
-MEASURED_TRAFFIC = {("das-wave-step-bf16", "a6750e5d3313a88c"): 4_467_663_082,
-                    ("long-prefix-gqa-bf16", "a6750e5d3313a88c"): 309_769_730,
-                    ("ragged-paged-bf16", "a6750e5d3313a88c"): 834_076_847,
-                    ("single-seq-looped-bf16", "a6750e5d3313a88c"): 47_032_309}
+MEASURED_TRAFFIC = {("das-wave-step-bf16", "075d852808585fb9"): 4_467_824_540,
+                    ("long-prefix-gqa-bf16", "075d852808585fb9"): 309_681_638,
+                    ("ragged-paged-bf16", "075d852808585fb9"): 834_118_830,
+                    ("single-seq-looped-bf16", "075d852808585fb9"): 47_018_211}
 
 
 def kernel_digest():

@@ -367,7 +367,7 @@ void attn_mfma_kernel(AttnParams p, int n_rg, int n_chunks) {
     }
     // the slot's fragments are in registers before the next barrier
     __builtin_amdgcn_s_waitcnt(0xF | (0x3 << 14) | (0x7 << 4));  // lgkmcnt(0)
-    compute_tile<DH, NQ, true>(st, kf, vf, qf, cap, limit, full, p.scale_log2, lg, [](int) {});
+    compute_tile<DH, NQ>(st, kf, vf, qf, cap, limit, full, p.scale_log2, lg, [](int) {});
   }
 
   }

@@ -152,14 +152,7 @@ struct State {
 // (every token visible) skips the mask.
 // `hook(k)` runs between the stages (k = 0 before the logits, 1 before the
 // softmax, 2 before P.V) so that the caller can spread work over the tile.
-// LAZY keeps a row's running maximum until a tile's maximum exceeds it by
-// more than kLazyLog2 (base 2): the probabilities then stay below 2^kLazyLog2
-// and the accumulators are rescaled only on such a jump, which after a row's
-// first tiles is rare (the softmax is the same up to rounding: l and O carry
-// the same factor). Otherwise the maximum always moves, so the row's largest
-// probability is exactly 1.
-constexpr float kLazyLog2 = 8.f;
-template <int DH, int NQ, bool LAZY = false, typename Hook>
+template <int DH, int NQ, typename Hook>
 __device__ __forceinline__ void compute_tile(State<DH, NQ> &st, const u32x4 (&kf)[2][DH / 32],
                                              const u32x4 (&vf)[DH / 16],
                                              const u32x4 (&qf)[NQ][DH / 32],
@@ -207,11 +200,10 @@ __device__ __forceinline__ void compute_tile(State<DH, NQ> &st, const u32x4 (&kf
     for (int e = 0; e < 2; ++e)
 #pragma unroll
       for (int v = 0; v < 4; ++v) mx = fmaxf(mx, x[e][v]);
-    // Running maximum (base-2 units): without LAZY the row's largest
-    // probability is exactly 1 and those near it fall just below, where bf16
-    // rounds finest.
+    // Running maximum (base-2 units): the row's largest probability is
+    // exactly 1 and those near it fall just below, where bf16 rounds finest.
     mx = group_max(mx) * scale;
-    const float mnew = LAZY ? (mx > st.m[qt] + kLazyLog2 ? mx : st.m[qt]) : fmaxf(st.m[qt], mx);
+    const float mnew = fmaxf(st.m[qt], mx);
     const float neg = mnew == kNegInf ? 0.f : -mnew;  // nothing visible yet: every p is 0
     alpha[qt] = __builtin_amdgcn_exp2f(st.m[qt] + neg);
     moved |= alpha[qt] != 1.f;

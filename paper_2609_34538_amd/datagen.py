@@ -88,7 +88,7 @@ WORKLOADS: Dict[int, Workload] = {
     3: Workload(3, "ragged-paged-bf16", torch.bfloat16, 16, 55, 55, 96, 32, 4, (512, 4096), (2,),
                 (16,), 16, 0.2, paged_random=True, append_max=16),
     4: Workload(4, "long-prefix-gqa-bf16", torch.bfloat16, 4, 32, 8, 128, 24, 4, (16384, 16384),
-                (3,), (32,), 32, 0.15, k_gain=3.0, append_max=32),
+                (3,), (32,), 32, 0.15, k_gain=3.0, append_max=32, residency="full"),
     5: Workload(5, "das-wave-step-bf16", torch.bfloat16, 32, 55, 55, 96, 32, 4, (4096, 8192),
                 (1, 2, 3, 4), (4, 8, 16, 32), 32, 0.2, paged_random=True, append_max=32),
 }
