@@ -238,21 +238,17 @@ void attn_mfma_kernel(AttnParams p, int n_rg, int n_chunks) {
     for (int dt = 0; dt < DT; ++dt) st.o[qt][dt] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  if constexpr (NW == 1) {
-  const bool long_chunk = ntile > kLongChunkTiles;
-  for (int t = 0; t < ntile; ++t) {
-    if (long_chunk) prio_by_remaining(ntile - t);
-    wait_tiles<NF>(n_issued - t - 1);
+  // Tile t's fragments from its ring slot into registers (keys; values as
+  // V^T fragments, the draft block's token-major values gathered), and which
+  // of its tokens each row sees.
+  auto read_tile = [&](int t, u32x4 (&kf)[2][KS], u32x4 (&vf)[DT], int (&cap)[NQ], int &limit,
+                       bool &full) {
     const uint8_t *slot = ring + (t % NB) * G::SLOT;
-    u32x4 kf[2][KS], vf[DT];
 #pragma unroll
     for (int e = 0; e < 2; ++e)
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks)
         kf[e][ks] = *reinterpret_cast<const u32x4 *>(slot + (e * KS + ks) * kFragBytes + 16 * lane);
-    int cap[NQ];
-    int limit;
-    bool full;
     if (t < npg2) {
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)
@@ -292,6 +288,18 @@ void attn_mfma_kernel(AttnParams p, int n_rg, int n_chunks) {
 #pragma unroll
       for (int qt = 0; qt < NQ; ++qt) cap[qt] = cap_blk[qt] - 32 * u;
     }
+  };
+
+  if constexpr (NW == 1) {
+  const bool long_chunk = ntile > kLongChunkTiles;
+  for (int t = 0; t < ntile; ++t) {
+    if (long_chunk) prio_by_remaining(ntile - t);
+    wait_tiles<NF>(n_issued - t - 1);
+    u32x4 kf[2][KS], vf[DT];
+    int cap[NQ];
+    int limit;
+    bool full;
+    read_tile(t, kf, vf, cap, limit, full);
     // the slot's fragments are in registers before it is refilled
     __builtin_amdgcn_s_waitcnt(0xF | (0x3 << 14) | (0x7 << 4));  // lgkmcnt(0)
     const int next = n_issued;
@@ -316,55 +324,11 @@ void attn_mfma_kernel(AttnParams p, int n_rg, int n_chunks) {
       for (int part = 0; part < 3; ++part) issue_part(n_issued, part, kbase, vbase);
       ++n_issued;
     }
-    const uint8_t *slot = ring + (t % NB) * G::SLOT;
     u32x4 kf[2][KS], vf[DT];
-#pragma unroll
-    for (int e = 0; e < 2; ++e)
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
-        kf[e][ks] = *reinterpret_cast<const u32x4 *>(slot + (e * KS + ks) * kFragBytes + 16 * lane);
     int cap[NQ];
     int limit;
     bool full;
-    if (t < npg2) {
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
-        vf[dt] = *reinterpret_cast<const u32x4 *>(slot + (2 * KS + dt) * kFragBytes + 16 * lane);
-      const int page = __builtin_amdgcn_readlane(page_id, t >> 1);
-      const bool ok = page >= 0 && page < p.num_pages;
-      limit = ok ? min(32, S - (pg0 + (t >> 1)) * kPage - 32 * (t & 1)) : 0;
-      full = limit >= 32;
-      if (!full) {
-        // Invisible tokens (past the prefix, or an unreadable page) enter P.V
-        // with probability 0; their values are zeroed so that whatever the
-        // cache holds there (NaN, Inf) contributes nothing. Lane group lg
-        // holds tokens 8 lg .. 8 lg + 7 of the tile, two per 32-bit word.
-        const int nv = min(max(limit - 8 * lg, 0), 8);
-        u32x4 keep;
-#pragma unroll
-        for (int k = 0; k < 4; ++k)
-          keep[k] = (2 * k < nv ? 0xffffu : 0u) | (2 * k + 1 < nv ? 0xffff0000u : 0u);
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) vf[dt] &= keep;
-      }
-#pragma unroll
-      for (int qt = 0; qt < NQ; ++qt) cap[qt] = 0x7fffffff;
-    } else {
-      // block values are token-major [32][DH] in the slot: gather V^T
-      const int u = t - npg2;
-      const uint16_t *raw = reinterpret_cast<const uint16_t *>(slot + 2 * KS * kFragBytes);
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        u16x8 v8;
-#pragma unroll
-        for (int jj = 0; jj < 8; ++jj) v8[jj] = raw[(8 * lg + jj) * DH + 16 * dt + ln];
-        vf[dt] = __builtin_bit_cast(u32x4, v8);
-      }
-      limit = p.w - 32 * u;
-      full = false;
-#pragma unroll
-      for (int qt = 0; qt < NQ; ++qt) cap[qt] = cap_blk[qt] - 32 * u;
-    }
+    read_tile(t, kf, vf, cap, limit, full);
     // the slot's fragments are in registers before the next barrier
     __builtin_amdgcn_s_waitcnt(0xF | (0x3 << 14) | (0x7 << 4));  // lgkmcnt(0)
     compute_tile<DH, NQ>(st, kf, vf, qf, cap, limit, full, p.scale_log2, lg, [](int) {});
