@@ -160,7 +160,7 @@ __device__ __forceinline__ void compute_tile(State<DH, NQ> &st, const u32x4 (&kf
                                              float scale, int lg, Hook &&hook) {
   u16x8 pf[NQ];
   float alpha[NQ];
-  bool moved = false;
+  bool moved[NQ];
   f32x4 sacc[NQ][2];
   hook(0);
   // k-step outermost: the 2 * NQ accumulators are independent, so no MFMA
@@ -206,7 +206,7 @@ __device__ __forceinline__ void compute_tile(State<DH, NQ> &st, const u32x4 (&kf
     const float mnew = fmaxf(st.m[qt], mx);
     const float neg = mnew == kNegInf ? 0.f : -mnew;  // nothing visible yet: every p is 0
     alpha[qt] = __builtin_amdgcn_exp2f(st.m[qt] + neg);
-    moved |= alpha[qt] != 1.f;
+    moved[qt] = alpha[qt] != 1.f;
     float psum = 0.f;
 #pragma unroll
     for (int e = 0; e < 2; ++e) {
@@ -222,12 +222,14 @@ __device__ __forceinline__ void compute_tile(State<DH, NQ> &st, const u32x4 (&kf
     st.m[qt] = mnew;
   }
   hook(2);
-  // rescale the accumulators only when some row's maximum moved
-  if (__builtin_amdgcn_ballot_w64(moved) != 0) {
+  // rescale a row tile's accumulators only when the maximum of one of its
+  // rows moved (a lane's accumulators of row tile qt all belong to one row)
 #pragma unroll
-    for (int qt = 0; qt < NQ; ++qt)
+  for (int qt = 0; qt < NQ; ++qt) {
+    if (__builtin_amdgcn_ballot_w64(moved[qt]) != 0) {
 #pragma unroll
       for (int dt = 0; dt < DH / 16; ++dt) st.o[qt][dt] *= alpha[qt];
+    }
   }
 #pragma unroll
   for (int dt = 0; dt < DH / 16; ++dt) {
