@@ -54,10 +54,10 @@ TRAFFIC_SOURCES = ["paper_2609_34538_amd/csrc/attn_mfma.hip",
                    "paper_2609_34538_amd/csrc/mfma_tile.h",
                    "paper_2609_34538_amd/csrc/das_api.hip",
                    "paper_2609_34538_amd/csrc/das_internal.h"]
-MEASURED_TRAFFIC = {("das-wave-step-bf16", "479d96b5075f6e56"): 4_467_845_328,
-                    ("long-prefix-gqa-bf16", "479d96b5075f6e56"): 309_651_718,
-                    ("ragged-paged-bf16", "479d96b5075f6e56"): 834_062_310,
-                    ("single-seq-looped-bf16", "479d96b5075f6e56"): 47_018_024}
+MEASURED_TRAFFIC = {("das-wave-step-bf16", "63073964926888c3"): 4_467_742_518,
+                    ("long-prefix-gqa-bf16", "63073964926888c3"): 309_656_663,
+                    ("ragged-paged-bf16", "63073964926888c3"): 834_106_126,
+                    ("single-seq-looped-bf16", "63073964926888c3"): 47_018_509}
 
 
 def kernel_digest():
