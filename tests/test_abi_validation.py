@@ -307,6 +307,10 @@ def test_balanced_schedule_workspace_and_limits():
     for B, path in ((17, 3), (16, 2)):
         bb = make_batch(B=B, maxp=10)
         assert ws_bytes(c128, bb, hq=8, w=16, opts=o) == ws_bytes(c128, bb, hq=8, w=16, opts=_opts(path)), B
+    c64 = make_cache(hkv=8, dh=64)  # 1792 workers: more than 224 units
+    for B, path in ((29, 3), (28, 2)):
+        bb = make_batch(B=B, maxp=10)
+        assert ws_bytes(c64, bb, hq=16, w=16, opts=o) == ws_bytes(c64, bb, hq=16, w=16, opts=_opts(path)), B
     o.pages_per_split = 4
     big = make_batch(B=21, maxp=10)
     assert ws_bytes(c, big, hq=16, w=16, opts=o) == ws_bytes(c, big, hq=16, w=16, opts=_opts(2, 4))
