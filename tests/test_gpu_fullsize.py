@@ -77,6 +77,15 @@ def test_config4_long_prefix_gqa_full():
     assert 2.7 <= logits.std() <= 3.3, logits.std()
     for layer in (0, 3):
         _check_rounds(cd, layer, list(range(wl.batch)), [(3, 32)])
+    # every depth is stored: the verifier sweep's Aligned reads at shallower
+    # depths (Sec. 3.4) on the full cache
+    cache, batch = wrap(cd)
+    for r in (1, 12):
+        q, kb, vb = dg.block_inputs(cd, wl.verify_width, r, DEV)
+        out = das.attn_verify(cache, batch, 2, r, q, kb, vb)
+        torch.cuda.synchronize()
+        ref, _ = oracle_call(cd, 2, r, r, q, kb, vb, [0, 3])
+        assert_close(out[[0, 3]], ref, wl.dtype, f"{wl.name} verify depth {r} layer 2")
 
 
 def test_config5_das_wave_step_full():
