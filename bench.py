@@ -54,10 +54,10 @@ TRAFFIC_SOURCES = ["paper_2609_34538_amd/csrc/attn_mfma.hip",
                    "paper_2609_34538_amd/csrc/mfma_tile.h",
                    "paper_2609_34538_amd/csrc/das_api.hip",
                    "paper_2609_34538_amd/csrc/das_internal.h"]
-MEASURED_TRAFFIC = {("das-wave-step-bf16", "63073964926888c3"): 4_467_742_518,
-                    ("long-prefix-gqa-bf16", "63073964926888c3"): 309_656_663,
-                    ("ragged-paged-bf16", "63073964926888c3"): 834_106_126,
-                    ("single-seq-looped-bf16", "63073964926888c3"): 47_018_509}
+MEASURED_TRAFFIC = {("das-wave-step-bf16", "59b3fe60afc333be"): 4_467_712_721,
+                    ("long-prefix-gqa-bf16", "59b3fe60afc333be"): 309_750_353,
+                    ("ragged-paged-bf16", "59b3fe60afc333be"): 834_107_912,
+                    ("single-seq-looped-bf16", "59b3fe60afc333be"): 47_019_461}
 
 
 def kernel_digest():

@@ -307,7 +307,7 @@ void attn_mfma_kernel(AttnParams p, int n_rg, int n_chunks) {
     if (refill) ++n_issued;
     const char *kbase = kl, *vbase = vl;
     if (refill && next < npg2) tile_src(next, kbase, vbase);
-    compute_tile<DH, NQ>(st, kf, vf, qf, cap, limit, full, p.scale_log2, lg, [&](int part) {
+    compute_tile<DH, NQ, true>(st, kf, vf, qf, cap, limit, full, p.scale_log2, lg, [&](int part) {
       if (refill) issue_part(next, part, kbase, vbase);
     });
   }
@@ -331,7 +331,7 @@ void attn_mfma_kernel(AttnParams p, int n_rg, int n_chunks) {
     read_tile(t, kf, vf, cap, limit, full);
     // the slot's fragments are in registers before the next barrier
     __builtin_amdgcn_s_waitcnt(0xF | (0x3 << 14) | (0x7 << 4));  // lgkmcnt(0)
-    compute_tile<DH, NQ>(st, kf, vf, qf, cap, limit, full, p.scale_log2, lg, [](int) {});
+    compute_tile<DH, NQ, true>(st, kf, vf, qf, cap, limit, full, p.scale_log2, lg, [](int) {});
   }
 
   }
@@ -343,8 +343,9 @@ void attn_mfma_kernel(AttnParams p, int n_rg, int n_chunks) {
   for (int qt = 0; qt < NQ; ++qt) {
     const int row = rt * ROWS + qt * 16 + ln;
     if (row >= p.rows) continue;
+    const float lrow = group_sum(st.l[qt]);  // row sum from its 4 lanes, all live
     if (nsb == 1) {
-      const float inv = 1.f / st.l[qt];
+      const float inv = 1.f / lrow;
       const int i = row / p.group, h = kvh * p.group + row % p.group;
       bf16_t *orow = static_cast<bf16_t *>(p.out) +
                      ((static_cast<size_t>(b) * p.w + i) * p.hq + h) * DH;
@@ -360,9 +361,9 @@ void attn_mfma_kernel(AttnParams p, int n_rg, int n_chunks) {
       }
       if (lg == 0 && p.lse)
         p.lse[(static_cast<size_t>(b) * p.hq + h) * p.w + i] =
-            (st.m[qt] + log2f(st.l[qt])) * 0.69314718055994530942f;
+            (st.m[qt] + log2f(lrow)) * 0.69314718055994530942f;
     } else {
-      write_piece_row<DH>(prec, p.rows, row, lg, st.o[qt], st.m[qt], st.l[qt]);
+      write_piece_row<DH>(prec, p.rows, row, lg, st.o[qt], st.m[qt], lrow);
     }
   }
 }

@@ -152,7 +152,10 @@ struct State {
 // (every token visible) skips the mask.
 // `hook(k)` runs between the stages (k = 0 before the logits, 1 before the
 // softmax, 2 before P.V) so that the caller can spread work over the tile.
-template <int DH, int NQ, typename Hook>
+// LANE_SUM: st.l holds this lane's share of its row's sum (alpha is the same
+// in a row's 4 lanes), which the caller reduces over the 4 lanes when it
+// writes the row; otherwise st.l holds the row's sum after every tile.
+template <int DH, int NQ, bool LANE_SUM = false, typename Hook>
 __device__ __forceinline__ void compute_tile(State<DH, NQ> &st, const u32x4 (&kf)[2][DH / 32],
                                              const u32x4 (&vf)[DH / 16],
                                              const u32x4 (&qf)[NQ][DH / 32],
@@ -217,7 +220,7 @@ __device__ __forceinline__ void compute_tile(State<DH, NQ> &st, const u32x4 (&kf
         pf[qt][4 * e + v] = __builtin_bit_cast(uint16_t, static_cast<__bf16>(pv));
       }
     }
-    psum = group_sum(psum);
+    if (!LANE_SUM) psum = group_sum(psum);
     st.l[qt] = st.l[qt] * alpha[qt] + psum;
     st.m[qt] = mnew;
   }
