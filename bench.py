@@ -54,10 +54,10 @@ TRAFFIC_SOURCES = ["paper_2609_34538_amd/csrc/attn_mfma.hip",
                    "paper_2609_34538_amd/csrc/mfma_tile.h",
                    "paper_2609_34538_amd/csrc/das_api.hip",
                    "paper_2609_34538_amd/csrc/das_internal.h"]
-MEASURED_TRAFFIC = {("das-wave-step-bf16", "59b3fe60afc333be"): 4_467_712_721,
-                    ("long-prefix-gqa-bf16", "59b3fe60afc333be"): 309_750_353,
-                    ("ragged-paged-bf16", "59b3fe60afc333be"): 834_107_912,
-                    ("single-seq-looped-bf16", "59b3fe60afc333be"): 47_019_461}
+MEASURED_TRAFFIC = {("das-wave-step-bf16", "8c10ff5ae1b54562"): 4_467_655_546,
+                    ("long-prefix-gqa-bf16", "8c10ff5ae1b54562"): 310_069_010,
+                    ("ragged-paged-bf16", "8c10ff5ae1b54562"): 834_019_002,
+                    ("single-seq-looped-bf16", "8c10ff5ae1b54562"): 47_022_823}
 
 
 def kernel_digest():

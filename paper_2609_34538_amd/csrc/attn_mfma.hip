@@ -219,6 +219,31 @@ void attn_mfma_kernel(AttnParams p, int n_rg, int n_chunks) {
     }
   };
 
+  // A shared-ring wave's loads of prefix tile t: its own block of NF / NW
+  // fragments, which is whole key halves or whole value groups, so the
+  // fragment offsets are scalars and no per-fragment test is made.
+  auto issue_own_prefix = [&](int t, const char *kbase, const char *vbase) {
+    constexpr int FPW = NF / NW;
+    static_assert(NW == 1 || (2 * KS) % FPW == 0, "a wave loads keys only or values only");
+    uint8_t *slot = ring + (t % NB) * G::SLOT;
+    const int f0 = wave * FPW;
+    if (f0 < 2 * KS) {
+      const auto r = buffer_of(kbase, 64 * DH);
+#pragma unroll
+      for (int i = 0; i < FPW; ++i) {
+        const int f = f0 + i, part = f / KS, ks = f - part * KS;
+        dma16(r, lane_k, (4 * part * DH + 32 * ks) * 2, slot + f * kFragBytes);
+      }
+    } else {
+      const auto r = buffer_of(vbase, 64 * DH);
+#pragma unroll
+      for (int i = 0; i < FPW; ++i) {
+        const int dt = f0 - 2 * KS + i;
+        dma16(r, lane_v, 256 * dt, slot + (2 * KS + dt) * kFragBytes);
+      }
+    }
+  };
+
   int n_issued = 0;
   for (; n_issued < NB && n_issued < ntile; ++n_issued) {
     const char *kbase = kl, *vbase = vl;
@@ -320,8 +345,12 @@ void attn_mfma_kernel(AttnParams p, int n_rg, int n_chunks) {
     __syncthreads();
     if (t >= 1 && n_issued < ntile) {
       const char *kbase = kl, *vbase = vl;
-      if (n_issued < npg2) tile_src(n_issued, kbase, vbase);
-      for (int part = 0; part < 3; ++part) issue_part(n_issued, part, kbase, vbase);
+      if (n_issued < npg2) {
+        tile_src(n_issued, kbase, vbase);
+        issue_own_prefix(n_issued, kbase, vbase);
+      } else {
+        for (int part = 0; part < 3; ++part) issue_part(n_issued, part, kbase, vbase);
+      }
       ++n_issued;
     }
     u32x4 kf[2][KS], vf[DT];
