@@ -69,9 +69,10 @@ __device__ __forceinline__ void prio_by_remaining(int rem) {
 // instead of being copied out of AGPRs on every tile.
 // NW = 1: one wave per chunk, its own ring. NW > 1: the NW row tiles of a
 // split share one workgroup and one ring; each wave loads its own block of
-// NF / NW consecutive fragments of a tile (whole 128-byte lines of the page) and one barrier per tile both publishes the tile and
-// frees the slot read in the previous iteration, which is then refilled
-// (NB - 1 tiles in flight).
+// NF / NW consecutive fragments of a tile (whole 128-byte lines of the
+// page), and one barrier per tile both publishes the tile and frees the slot
+// read in the previous iteration, which is then refilled (NB - 1 tiles in
+// flight).
 template <int DH, int NQ, int NB, int NW>
 __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(2)))
 void attn_mfma_kernel(AttnParams p, int n_rg, int n_chunks) {
